@@ -1,0 +1,177 @@
+"""CPU oracle of the PACE filter step -- TEST INFRASTRUCTURE ONLY.
+
+A plain single-threaded C implementation (``pace_oracle.c``) of the paper's
+definitions, wrapped here with ctypes over numpy arrays. Only ``tests/``,
+``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
+import it. The GPU library does not import, link or call anything here, and
+nothing here imports the GPU library.
+
+Functions mirror the filter step: ``validate``, ``score`` (Eq. (1)-(2),
+(6)-(9)), ``budget`` (Eq. (3)-(4)), ``select`` (Sec. 3.1 rejection rule,
+exact count, ties to the lower id) and ``compact`` (Algorithm 1: survivors
+packed into the training batch).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pace_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+OK = 0
+ERR_ARG = -1
+ERR_PRECONDITION = -3
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (IEEE double, no contraction, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared",
+                               "-ffp-contract=off", "-fno-fast-math",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def load_library(path: str):
+    """Open an oracle shared object and declare its C signatures."""
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    i64, i32, d = ctypes.c_int64, ctypes.c_int32, ctypes.c_double
+    lib.oracle_validate.argtypes = [P, P, i64, i64, P, i32]
+    lib.oracle_score.argtypes = [P, P, i64, i64, P, i32, P, P, i64, d, i32, i64, P, P, P]
+    lib.oracle_budget.argtypes = [i64, i64, d, d, P, P]
+    lib.oracle_select.argtypes = [P, i64, i64, P, P]
+    lib.oracle_compact.argtypes = [P, i64, i64, P, ctypes.c_int, P, P, P, P, P, P]
+    for f in ("oracle_validate", "oracle_score", "oracle_budget", "oracle_select", "oracle_compact"):
+        getattr(lib, f).restype = ctypes.c_int
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        _lib = load_library(_LIB_PATH)
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__("%s failed with code %d" % (what, code))
+        self.code = code
+
+
+def _c(a, dt):
+    return np.ascontiguousarray(a, dtype=dt)
+
+
+def validate(tags, offsets, completion, V) -> int:
+    tags, offsets, completion = _c(tags, np.int32), _c(offsets, np.int64), _c(completion, np.int32)
+    n = offsets.shape[0] - 1
+    return _load().oracle_validate(_p(tags), _p(offsets), n, tags.shape[0], _p(completion), int(V))
+
+
+def score(tags, offsets, completion, V, prefix=None, window=None, w_wait=1.0,
+          gamma=4, window_min=32, check=True):
+    """Returns (score float64[n], S int64[n], T int64[n]) or raises."""
+    tags, offsets, completion = _c(tags, np.int32), _c(offsets, np.int64), _c(completion, np.int32)
+    n = offsets.shape[0] - 1
+    prefix = None if prefix is None else _c(prefix, np.float64)
+    window = np.empty(0) if window is None else _c(window, np.float64)
+    out = np.empty(n, np.float64)
+    S = np.empty(n, np.int64)
+    T = np.empty(n, np.int64)
+    rc = _load().oracle_score(_p(tags), _p(offsets), n, tags.shape[0], _p(completion), int(V),
+                              _p(prefix), _p(window), window.shape[0], float(w_wait), int(gamma),
+                              int(window_min), _p(out), _p(S), _p(T))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_score")
+        return rc
+    return out, S, T
+
+
+def budget(N, N_tar, r_hat_prev=0.0, beta=0.0, r_max=0.9, check=True):
+    """Returns (budget, r_hat)."""
+    rh = ctypes.c_double(float(r_hat_prev))
+    b = ctypes.c_int64(0)
+    rc = _load().oracle_budget(int(N), int(N_tar), float(beta), float(r_max),
+                               ctypes.addressof(rh), ctypes.addressof(b))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_budget")
+        return rc
+    return int(b.value), float(rh.value)
+
+
+def select(score_arr, budget_n, check=True):
+    """Returns (keep uint8[n], reject_ids int32[budget])."""
+    s = _c(score_arr, np.float64)
+    n = s.shape[0]
+    keep = np.empty(n, np.uint8)
+    rej = np.empty(max(int(budget_n), 0), np.int32)
+    rc = _load().oracle_select(_p(s), n, int(budget_n), _p(keep), _p(rej))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_select")
+        return rc
+    return keep, rej
+
+
+def compact(offsets, keep, cols: Sequence[np.ndarray], check=True):
+    """Returns (offsets_out int64[n_kept+1], kept_ids int32[n_kept], packed cols)."""
+    offsets = _c(offsets, np.int64)
+    keep = _c(keep, np.uint8)
+    n = offsets.shape[0] - 1
+    cols = [np.ascontiguousarray(c) for c in cols]
+    n_tokens = int(cols[0].shape[0]) if cols else int(offsets[-1])
+    outs = [np.empty_like(c) for c in cols]
+    nc = len(cols)
+    cin = (ctypes.c_void_p * max(nc, 1))(*[c.ctypes.data for c in cols])
+    cout = (ctypes.c_void_p * max(nc, 1))(*[o.ctypes.data for o in outs])
+    eb = (ctypes.c_int32 * max(nc, 1))(*[c.dtype.itemsize for c in cols])
+    off_out = np.empty(n + 1, np.int64)
+    ids = np.empty(max(n, 1), np.int32)
+    nk = ctypes.c_int64(0)
+    rc = _load().oracle_compact(_p(offsets), n, n_tokens, _p(keep), nc, cin, eb, cout,
+                                _p(off_out), _p(ids), ctypes.addressof(nk))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_compact")
+        return rc
+    n_kept = int(keep.astype(bool).sum())
+    tot = int(nk.value)
+    return off_out[: n_kept + 1].copy(), ids[:n_kept].copy(), [o[:tot].copy() for o in outs]
+
+
+def filter_step(pool, mode="effective", w_wait=None, gamma=4, window_min=32,
+                beta=0.0, r_max=0.9, r_hat_prev=0.0, cols=None):
+    """One whole filter step on a poolgen.Pool: score -> budget -> select -> compact.
+    mode: 'effective' (Eq. (7)), 'raw' (F = 1) or 'gen' (w_wait = 0, Eq. (7) weight)."""
+    prefix = None if mode == "raw" else pool.prefix_score
+    window = None if mode == "raw" else pool.window
+    if w_wait is None:
+        w_wait = 0.0 if mode == "gen" else 1.0
+    sc, S, T = score(pool.tags, pool.offsets, pool.completion, pool.V, prefix, window,
+                     w_wait, gamma, window_min)
+    b, r_hat = budget(pool.occupancy, pool.capacity, r_hat_prev, beta, r_max)
+    keep, rej = select(sc, b)
+    cols = [pool.tags] if cols is None else cols
+    off_out, ids, packed = compact(pool.offsets, keep, cols)
+    return dict(score=sc, S=S, T=T, budget=b, r_hat=r_hat, keep=keep, reject_ids=rej,
+                offsets_out=off_out, kept_ids=ids, packed=packed,
+                n_kept_tokens=int(off_out[-1]))

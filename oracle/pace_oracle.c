@@ -1,0 +1,270 @@
+/*
+ * PACE filter step -- CPU ORACLE (test infrastructure only).
+ *
+ * A plain, slow, single-threaded reference of what the filter step computes,
+ * written from the paper's definitions. Only the test suite, the smoke check
+ * and the benchmark's CPU-baseline leg load it. It shares no source, header,
+ * table or helper with the GPU library, and the GPU library never calls it.
+ *
+ * Every floating-point expression is evaluated in IEEE binary64 with
+ * round-to-nearest, one operation at a time (built with -ffp-contract=off and
+ * without fast-math), in the order written here.
+ *
+ * Readings of the paper that this file adopts (where it is silent):
+ *   - a token tagged -1 is non-generated (tool output): it is not one of the
+ *     T response tokens of Eq. (1), so it is excluded from T and from the
+ *     staleness sums, but it stays in the trajectory's span when compacted;
+ *   - T = 0 gives Generation Staleness 0;
+ *   - the empirical CDF of Eq. (8) counts window entries <= s;
+ *   - gamma is an integer in [1,4], so phi_gamma(a/W) is evaluated exactly
+ *     as a^g / (a^g + (W-a)^g) and rounded once;
+ *   - a missing prefix score (NaN), no window, or fewer than window_min
+ *     observations gives F = 1 (the full Generation Staleness penalty);
+ *   - the rejection budget is an integer count: rint(min(r_hat, r_max) * N),
+ *     forced to 0 when N <= N^tar and capped at the surplus N - N^tar;
+ *   - the quantile rule "reject M > kappa" is taken over the current pool
+ *     with exactly `budget` rejections; equal scores reject the lower
+ *     trajectory id first.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_ERR_ARG (-1)
+#define ORC_ERR_PRECONDITION (-3)
+
+/* ------------------------------------------------------------------------
+ * Preconditions of Lemma 1: every generated token's version v_t satisfies
+ * v_t <= c(tau) <= j (Sec. 2, Lemma 1 and its proof in App. A), versions are
+ * non-negative indices, and the CSR offsets describe the token array.
+ * ---------------------------------------------------------------------- */
+int oracle_validate(const int32_t *tags, const int64_t *offsets, int64_t n,
+                    int64_t n_tokens, const int32_t *completion, int32_t V)
+{
+    if (n < 0 || n_tokens < 0 || !offsets || (n > 0 && !completion) ||
+        (n_tokens > 0 && !tags))
+        return ORC_ERR_ARG;
+    if (offsets[0] != 0 || offsets[n] != n_tokens)
+        return ORC_ERR_PRECONDITION;
+    for (int64_t i = 0; i < n; i++) {
+        if (offsets[i + 1] < offsets[i])
+            return ORC_ERR_PRECONDITION;
+        int32_t c = completion[i];
+        if (c < 0 || c > V)
+            return ORC_ERR_PRECONDITION;
+        for (int64_t t = offsets[i]; t < offsets[i + 1]; t++) {
+            int32_t v = tags[t];
+            if (v == -1)
+                continue;
+            if (v < 0 || v > c)
+                return ORC_ERR_PRECONDITION;
+        }
+    }
+    return ORC_OK;
+}
+
+/* Integer power for the exact form of phi_gamma. */
+static int64_t ipow(int64_t x, int g)
+{
+    int64_t r = 1;
+    for (int k = 0; k < g; k++)
+        r *= x;
+    return r;
+}
+
+/* ------------------------------------------------------------------------
+ * Scores, Sec. 2 and Sec. 3.2.
+ *
+ * For trajectory i with completion version c_i, consumed at version j = V:
+ *   T_i       = number of generated (tag != -1) tokens          (Eq. (1))
+ *   S_i       = sum over those tokens of (c_i - v_t)            (Eq. (2))
+ *   K_gen     = S_i / T_i   (0 when T_i = 0)                     (Eq. (2))
+ *   K_wait    = V - c_i                                          (Eq. (2))
+ *   q         = #{w in window : w <= s_pre} / W                  (Eq. (8))
+ *   F         = phi_gamma(q) = q^g / (q^g + (1-q)^g)             (Eq. (9))
+ *   M         = w_wait * K_wait + F * K_gen                     (Eq. (6),(7))
+ * With prefix == NULL the weight is F = 1: PACE (Raw Staleness), whose score
+ * equals the trajectory lag of Eq. (1). With w_wait = 0 it is the
+ * generation-only variant (Sec. 3.2, "Other Variants").
+ * ---------------------------------------------------------------------- */
+int oracle_score(const int32_t *tags, const int64_t *offsets, int64_t n,
+                 int64_t n_tokens, const int32_t *completion, int32_t V,
+                 const double *prefix, const double *window, int64_t W,
+                 double w_wait, int32_t gamma, int64_t window_min,
+                 double *score_out, int64_t *S_out, int64_t *T_out)
+{
+    if (!score_out || gamma < 1 || gamma > 4 || window_min < 0 || W < 0 ||
+        !(w_wait >= 0.0) || isinf(w_wait) || (W > 0 && !window))
+        return ORC_ERR_ARG;
+    /* the exact form needs W^gamma representable in a double */
+    if (W > 0 && (double)ipow(W, gamma) >= 9007199254740992.0)
+        return ORC_ERR_ARG;
+    int rc = oracle_validate(tags, offsets, n, n_tokens, completion, V);
+    if (rc != ORC_OK)
+        return rc;
+    for (int64_t k = 1; k < W; k++)
+        if (!(window[k - 1] <= window[k]))
+            return ORC_ERR_PRECONDITION;   /* window must be sorted, no NaN */
+    if (W > 0 && isnan(window[0]))
+        return ORC_ERR_PRECONDITION;
+
+    for (int64_t i = 0; i < n; i++) {
+        int64_t c = completion[i];
+        int64_t T = 0, S = 0;
+        for (int64_t t = offsets[i]; t < offsets[i + 1]; t++) {
+            int32_t v = tags[t];
+            if (v == -1)
+                continue;            /* non-generated token */
+            T += 1;
+            S += c - (int64_t)v;
+        }
+        double K_wait = (double)((int64_t)V - c);
+        double K_gen = (T > 0) ? (double)S / (double)T : 0.0;
+
+        double F = 1.0;
+        if (prefix && W > 0 && W >= window_min && !isnan(prefix[i])) {
+            int64_t a = 0;
+            for (int64_t k = 0; k < W; k++)
+                if (window[k] <= prefix[i])
+                    a += 1;
+            int64_t A = ipow(a, gamma);
+            int64_t B = ipow(W - a, gamma);
+            F = (double)A / (double)(A + B);
+        }
+        double wait_term = w_wait * K_wait;
+        double gen_term = F * K_gen;
+        score_out[i] = wait_term + gen_term;
+        if (S_out)
+            S_out[i] = S;
+        if (T_out)
+            T_out[i] = T;
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Rejection budget, Sec. 3.1.
+ *   r_j    = clip((N - N^tar) / max(N, 1), 0, 1)                 (Eq. (3))
+ *   r_hat  = beta * r_hat_prev + (1 - beta) * r_j                (Eq. (4))
+ *   budget = 0 if N <= N^tar, else
+ *            min(rint(min(r_hat, r_max) * N), N - N^tar)
+ * r_max is the maximum rejection budget of App. B (0.9 there).
+ * ---------------------------------------------------------------------- */
+int oracle_budget(int64_t N, int64_t N_tar, double beta, double r_max,
+                  double *r_hat_inout, int64_t *budget_out)
+{
+    if (!r_hat_inout || !budget_out || N < 0 || N_tar < 0 ||
+        !(beta >= 0.0 && beta < 1.0) || !(r_max >= 0.0 && r_max <= 1.0) ||
+        !(*r_hat_inout >= 0.0) || isinf(*r_hat_inout))
+        return ORC_ERR_ARG;
+    double denom = (double)(N > 1 ? N : 1);
+    double x = (double)(N - N_tar) / denom;
+    double r = x < 0.0 ? 0.0 : (x > 1.0 ? 1.0 : x);
+    double r_hat = beta * (*r_hat_inout) + (1.0 - beta) * r;
+    int64_t b = 0;
+    if (N > N_tar) {
+        double rc = r_hat < r_max ? r_hat : r_max;
+        b = (int64_t)nearbyint(rc * (double)N);   /* default mode: ties to even */
+        if (b > N - N_tar)
+            b = N - N_tar;
+        if (b < 0)
+            b = 0;
+    }
+    *r_hat_inout = r_hat;
+    *budget_out = b;
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Selection, Sec. 3.1 and Algorithm 1 (trainer side): the trajectories with
+ * the highest scores are rejected. Here exactly `budget` of them: sort all
+ * ids by (score descending, id ascending) and reject the first `budget`.
+ * ---------------------------------------------------------------------- */
+static const double *g_sort_scores;   /* comparator context (single thread) */
+
+static int by_score_desc_id_asc(const void *pa, const void *pb)
+{
+    int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    double sa = g_sort_scores[a], sb = g_sort_scores[b];
+    if (sa > sb)
+        return -1;
+    if (sa < sb)
+        return 1;
+    return (a < b) ? -1 : (a > b);
+}
+
+int oracle_select(const double *score, int64_t n, int64_t budget,
+                  uint8_t *keep_out, int32_t *reject_ids_out)
+{
+    if (n < 0 || n > INT32_MAX || budget < 0 || budget > n ||
+        (n > 0 && (!score || !keep_out)) || (budget > 0 && !reject_ids_out))
+        return ORC_ERR_ARG;
+    for (int64_t i = 0; i < n; i++)
+        if (isnan(score[i]))
+            return ORC_ERR_PRECONDITION;
+    int32_t *order = (int32_t *)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    if (!order)
+        return ORC_ERR_ARG;
+    for (int64_t i = 0; i < n; i++)
+        order[i] = (int32_t)i;
+    g_sort_scores = score;
+    qsort(order, (size_t)n, sizeof(int32_t), by_score_desc_id_asc);
+    for (int64_t i = 0; i < n; i++)
+        keep_out[i] = 1;
+    for (int64_t r = 0; r < budget; r++)
+        keep_out[order[r]] = 0;
+    int64_t k = 0;
+    for (int64_t i = 0; i < n; i++)
+        if (!keep_out[i])
+            reject_ids_out[k++] = (int32_t)i;
+    free(order);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Compaction: the survivors form the training batch (Sec. 3.1, Algorithm 1).
+ * Kept trajectories stay in pool order; each payload column's kept spans are
+ * concatenated (non-generated tokens included, they stay in context).
+ * ---------------------------------------------------------------------- */
+int oracle_compact(const int64_t *offsets, int64_t n, int64_t n_tokens,
+                   const uint8_t *keep, int n_cols,
+                   const void *const *cols_in, const int32_t *elem_bytes,
+                   void *const *cols_out, int64_t *offsets_out,
+                   int32_t *kept_ids_out, int64_t *n_kept_tokens_out)
+{
+    if (n < 0 || n > INT32_MAX || !offsets || !offsets_out || !n_kept_tokens_out ||
+        n_cols < 0 || (n > 0 && (!keep || !kept_ids_out)) ||
+        (n_cols > 0 && (!cols_in || !cols_out || !elem_bytes)))
+        return ORC_ERR_ARG;
+    for (int c = 0; c < n_cols; c++) {
+        int32_t e = elem_bytes[c];
+        if (!(e == 1 || e == 2 || e == 4 || e == 8) || (n_tokens > 0 && (!cols_in[c] || !cols_out[c])))
+            return ORC_ERR_ARG;
+    }
+    if (offsets[0] != 0 || offsets[n] != n_tokens)
+        return ORC_ERR_PRECONDITION;
+    for (int64_t i = 0; i < n; i++)
+        if (offsets[i + 1] < offsets[i])
+            return ORC_ERR_PRECONDITION;
+
+    int64_t pos = 0, k = 0;
+    for (int64_t i = 0; i < n; i++) {
+        if (!keep[i])
+            continue;
+        int64_t len = offsets[i + 1] - offsets[i];
+        offsets_out[k] = pos;
+        kept_ids_out[k] = (int32_t)i;
+        for (int c = 0; c < n_cols; c++) {
+            size_t e = (size_t)elem_bytes[c];
+            memcpy((char *)cols_out[c] + (size_t)pos * e,
+                   (const char *)cols_in[c] + (size_t)offsets[i] * e, (size_t)len * e);
+        }
+        pos += len;
+        k += 1;
+    }
+    offsets_out[k] = pos;
+    *n_kept_tokens_out = pos;
+    return ORC_OK;
+}

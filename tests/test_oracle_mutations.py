@@ -1,0 +1,82 @@
+"""The pins must have teeth: plant plausible mistakes in copies of the CPU
+oracle (on the CPU only) and require that some pin in test_oracle_pins fails
+for every one of them. The real oracle is restored afterwards."""
+import subprocess
+
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+# (name, original text, mutated text) -- each a mistake one could make when
+# transcribing the paper's definitions.
+MUTATIONS = [
+    ("gen staleness sign flipped", "S += c - (int64_t)v;", "S += (int64_t)v - c;"),
+    ("mask tag not excluded", "if (v == -1)\n                continue;            /* non-generated token */",
+     "if (v == -2)\n                continue;"),
+    ("masked tokens counted in T", "continue;            /* non-generated token */",
+     "{ T += 1; continue; }"),
+    ("waiting term dropped", "score_out[i] = wait_term + gen_term;", "score_out[i] = gen_term;"),
+    ("waiting staleness sign flipped", "double K_wait = (double)((int64_t)V - c);",
+     "double K_wait = (double)(c - (int64_t)V);"),
+    ("K_gen operands transposed", "(double)S / (double)T : 0.0", "(double)T / ((double)S + 1.0) : 0.0"),
+    ("phi numerator transposed", "F = (double)A / (double)(A + B);", "F = (double)B / (double)(A + B);"),
+    ("ECDF strict instead of <=", "if (window[k] <= prefix[i])", "if (window[k] < prefix[i])"),
+    ("gamma ignored on complement", "int64_t B = ipow(W - a, gamma);", "int64_t B = ipow(W - a, 1);"),
+    ("F weight applied to waiting term", "double wait_term = w_wait * K_wait;\n        double gen_term = F * K_gen;",
+     "double wait_term = w_wait * F * K_wait;\n        double gen_term = K_gen;"),
+    ("EMA coefficients swapped", "double r_hat = beta * (*r_hat_inout) + (1.0 - beta) * r;",
+     "double r_hat = (1.0 - beta) * (*r_hat_inout) + beta * r;"),
+    ("rate normalised by target", "double x = (double)(N - N_tar) / denom;",
+     "double x = (double)(N - N_tar) / (double)(N_tar > 1 ? N_tar : 1);"),
+    ("budget floors instead of rounding", "b = (int64_t)nearbyint(rc * (double)N);", "b = (int64_t)floor(rc * (double)N);"),
+    ("no zero budget at target, no cap", "if (N > N_tar) {\n        double rc = r_hat < r_max ? r_hat : r_max;\n"
+     "        b = (int64_t)nearbyint(rc * (double)N);   /* default mode: ties to even */\n"
+     "        if (b > N - N_tar)\n            b = N - N_tar;",
+     "{\n        double rc = r_hat < r_max ? r_hat : r_max;\n        b = (int64_t)nearbyint(rc * (double)N);"),
+    ("surplus cap missing", "        if (b > N - N_tar)\n            b = N - N_tar;\n", ""),
+    ("max rejection cap missing", "double rc = r_hat < r_max ? r_hat : r_max;", "double rc = r_hat;"),
+    ("select ties to the higher id", "return (a < b) ? -1 : (a > b);", "return (a > b) ? -1 : (a < b);"),
+    ("select ascending", "if (sa > sb)\n        return -1;\n    if (sa < sb)\n        return 1;",
+     "if (sa < sb)\n        return -1;\n    if (sa > sb)\n        return 1;"),
+    ("select off by one", "for (int64_t r = 0; r < budget; r++)", "for (int64_t r = 1; r < budget; r++)"),
+    ("compact writes source offsets", "offsets_out[k] = pos;\n        kept_ids_out[k]",
+     "offsets_out[k] = offsets[i];\n        kept_ids_out[k]"),
+    ("compact copies from packed position", "(const char *)cols_in[c] + (size_t)offsets[i] * e",
+     "(const char *)cols_in[c] + (size_t)pos * e"),
+    ("validate checks tag against V", "if (v < 0 || v > c)", "if (v < 0 || v > V)"),
+]
+
+PIN_FUNCS = [getattr(pins, n) for n in dir(pins) if n.startswith("test_") and callable(getattr(pins, n))]
+
+
+def _run_pins():
+    failed = []
+    for f in PIN_FUNCS:
+        try:
+            f()
+        except Exception as e:   # assertion, oracle error, or hypothesis failure
+            failed.append((f.__name__, type(e).__name__))
+    return failed
+
+
+@pytest.mark.parametrize("name,old,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_planted_mistake_is_caught(name, old, new, tmp_path):
+    src = open(oracle._SRC).read()
+    assert src.count(old) == 1, "mutation anchor not found: " + name
+    mut = tmp_path / "mut.c"
+    mut.write_text(src.replace(old, new))
+    so = tmp_path / "libmut.so"
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-ffp-contract=off",
+                           "-o", str(so), str(mut), "-lm"])
+    real = oracle._load()
+    oracle._lib = oracle.load_library(str(so))
+    try:
+        failed = _run_pins()
+    finally:
+        oracle._lib = real
+    assert failed, "no pin caught the planted mistake: " + name
+
+
+def test_unmutated_oracle_passes_all_pins():
+    assert _run_pins() == []
