@@ -1,0 +1,188 @@
+/*
+ * pace.h -- C ABI of the PACE pool filter step on AMD Instinct MI355X (gfx950).
+ *
+ * PACE (Pool-Aware Control of Effective Staleness) filters the pool of
+ * completed asynchronous-RL trajectories before each trainer step:
+ *
+ *   pace_score    per-trajectory staleness score              Eq. (1),(2),(6)-(9)
+ *   pace_budget   occupancy-driven rejection budget            Eq. (3),(4)
+ *   pace_select   reject exactly `budget` highest scores       Sec. 3.1, Algorithm 1
+ *   pace_compact  pack the survivors' token spans              Algorithm 1 (batch B_j)
+ *   pace_validate check the data preconditions of Lemma 1     Sec. 2, Lemma 1
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pool layout (CSR over tokens): trajectory i owns tokens
+ *   [offsets[i], offsets[i+1]) of every per-token column. offsets has n_traj+1
+ *   int64 entries, offsets[0] = 0, non-decreasing, offsets[n_traj] = n_tokens.
+ * - Per-token version tags (int32): the behavior policy version v_t that
+ *   generated the token; -1 marks a non-generated token (tool output in a
+ *   multi-turn rollout). Masked tokens are not response tokens of Eq. (1): they
+ *   count neither in T nor in the staleness sums, but compaction copies them.
+ * - Pointers are DEVICE pointers unless marked [host]. Every device call is
+ *   enqueued on `stream` (a hipStream_t passed as void*, NULL = null stream)
+ *   and returns without synchronising. Nothing is allocated or freed inside a
+ *   call; the caller owns every buffer, including the workspace, and no
+ *   pointer is retained after a call returns. Inputs and outputs must not
+ *   overlap.
+ * - Argument errors the host can see (null required pointers, negative or
+ *   oversized counts, bad parameters, misaligned or short workspace) return
+ *   an error code before anything is enqueued and nothing is written.
+ * - Data preconditions (monotone offsets, -1 <= tag <= c_i, 0 <= c_i <= V,
+ *   sorted window) are NOT checked by the fast path: violating them gives
+ *   unspecified (but memory-safe, in-bounds) results. pace_validate checks
+ *   them on the device.
+ * - A failed kernel launch returns PACE_ERR_HIP.
+ * - Every result is a deterministic function of the inputs: identical bits
+ *   run to run and for any stream.
+ * - Workspace: at least pace_workspace_bytes() bytes, 256-byte aligned. Its
+ *   contents need no initialisation and are scratch between calls; calls
+ *   sharing one workspace must be ordered (same stream).
+ */
+#ifndef PACE_H
+#define PACE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PACE_OK 0
+#define PACE_ERR_INVALID_ARG (-1)
+#define PACE_ERR_WORKSPACE (-2)
+#define PACE_ERR_PRECONDITION (-3)
+#define PACE_ERR_HIP (-4)
+
+/* Bits of the device error word written by pace_validate. */
+#define PACE_BAD_OFFSETS 0x1    /* offsets[0] != 0, decreasing, or offsets[n] != n_tokens */
+#define PACE_BAD_COMPLETION 0x2 /* some c_i < 0 or c_i > current_version */
+#define PACE_BAD_TAG 0x4        /* some tag < -1, or tag > c_i of its trajectory */
+#define PACE_BAD_WINDOW 0x8     /* prefix window not ascending, or holds NaN */
+
+/* Controller parameters (host struct).
+ *   w_wait     w_1 of Eq. (6): 1 for Effective and Raw Staleness, 0 for the
+ *              generation-only variant (Sec. 3.2). Finite, >= 0.
+ *   gamma      sharpening exponent of Eq. (9); integer in [1,4] (4 by default,
+ *              App. B). window_n^gamma must stay below 2^53.
+ *   window_min minimum number of prefix-window observations before the
+ *              prefix weight applies (32, App. B); below it F = 1. >= 0.
+ *   beta       EMA coefficient of Eq. (4), in [0,1) (0 by default).
+ *   r_max      maximum rejection budget, in [0,1] (0.9, App. B). */
+typedef struct pace_params {
+    double w_wait;
+    int32_t gamma;
+    int32_t window_min;
+    double beta;
+    double r_max;
+} pace_params;
+
+/* Fills *p with the defaults above (w_wait 1, gamma 4, window_min 32, beta 0,
+ * r_max 0.9). */
+void pace_default_params(pace_params *p);
+
+/* Workspace sizes. `which` selects the call: */
+#define PACE_WS_SCORE 0
+#define PACE_WS_SELECT 1
+#define PACE_WS_COMPACT 2
+/* Writes to *bytes_out [host] the workspace that call needs for a pool of
+ * n_traj trajectories and n_tokens tokens. Returns PACE_ERR_INVALID_ARG for
+ * negative sizes or an unknown `which`. */
+int pace_workspace_bytes(int which, int64_t n_traj, int64_t n_tokens, size_t *bytes_out);
+
+/* pace_score -- per-trajectory effective-staleness score (Sec. 2, Sec. 3.2).
+ *
+ * For trajectory i with completion version c_i = completion[i], consumed at
+ * the current version j = current_version:
+ *   T_i    = number of tokens with tag != -1                   (Eq. (1))
+ *   S_i    = sum over those tokens of (c_i - tag)             (Eq. (2), K_gen = S_i/T_i)
+ *   K_wait = j - c_i                                           (Eq. (2))
+ *   F_i    = phi_gamma(q_i), q_i = #{w in window : w <= s_i} / W  (Eq. (8),(9))
+ *   M_i    = w_wait * K_wait + F_i * K_gen                     (Eq. (6),(7))
+ * evaluated as K_gen = (double)S_i / (double)T_i (0 when T_i = 0),
+ * F_i = (double)a^g / (double)(a^g + (W-a)^g), and
+ * M_i = (w_wait*K_wait) + (F_i*K_gen), each operation an IEEE binary64
+ * round-to-nearest step, never fused.
+ * F_i = 1 (PACE Raw Staleness) when prefix_score is NULL, when prefix_score[i]
+ * is NaN (no prefix score: the rollout was never interrupted), or when
+ * window_n < max(params->window_min, 1).
+ *
+ * tags          int32 [n_tokens], 16-byte aligned for the vector path
+ * offsets       int64 [n_traj+1]
+ * completion    int32 [n_traj]
+ * current_version  j; must be < 2^31 - 1
+ * prefix_score  double [n_traj] or NULL
+ * window_sorted double [window_n], ascending, or NULL when window_n = 0
+ * params        [host] controller parameters (NULL = defaults)
+ * score_out     double [n_traj]  (required)
+ * gen_sum_out   int64 [n_traj]   S_i, or NULL
+ * gen_count_out int64 [n_traj]   T_i, or NULL
+ * A single trajectory may hold at most 2^32 - 1 tokens. */
+int pace_score(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+               const int32_t *completion, int32_t current_version,
+               const double *prefix_score, const double *window_sorted, int64_t window_n,
+               const pace_params *params, double *score_out, int64_t *gen_sum_out,
+               int64_t *gen_count_out, void *workspace, size_t workspace_bytes, void *stream);
+
+/* pace_budget -- rejection budget from pool occupancy (Sec. 3.1). Host only.
+ *   r_j    = clip((N - N^tar) / max(N,1), 0, 1)                Eq. (3)
+ *   r_hat  = beta * r_hat_prev + (1 - beta) * r_j              Eq. (4)
+ *   budget = 0 if N <= N^tar, else min(rint(min(r_hat, r_max) * N), N - N^tar)
+ * (rint rounds half to even). occupancy N >= 0, capacity N^tar >= 0.
+ * r_hat_inout [host] holds r_hat_{j-1} on entry (finite, >= 0; 0 at the first
+ * step) and r_hat_j on return. budget_out [host]. */
+int pace_budget(int64_t occupancy, int64_t capacity, const pace_params *params,
+                double *r_hat_inout, int64_t *budget_out);
+
+/* pace_select -- reject exactly `budget` trajectories (Sec. 3.1, Algorithm 1).
+ * The rejected set is the first `budget` ids in the order (score descending,
+ * id ascending): trajectories with higher scores go first and equal scores
+ * reject the lower id first. -0.0 and +0.0 are equal. NaN scores violate the
+ * precondition (pace_score never produces them); they order above +inf.
+ * score          double [n_traj]
+ * budget         0 <= budget <= n_traj (n_traj < 2^31)
+ * keep_out       uint8 [n_traj]: 1 = kept, 0 = rejected
+ * reject_ids_out int32 [budget]: rejected ids, ascending (may be NULL when
+ *                budget = 0) */
+int pace_select(const double *score, int64_t n_traj, int64_t budget, uint8_t *keep_out,
+                int32_t *reject_ids_out, void *workspace, size_t workspace_bytes, void *stream);
+
+/* pace_compact -- pack the kept trajectories into the training batch
+ * (Algorithm 1). Kept trajectories stay in pool order; for every payload
+ * column the kept spans are concatenated (masked tokens included).
+ * offsets           int64 [n_traj+1]
+ * keep              uint8 [n_traj] (nonzero = kept)
+ * n_cols            0..8 payload columns, each n_tokens elements of
+ *                   elem_bytes[c] in {1,2,4,8} bytes
+ * cols_in, cols_out [host] arrays of n_cols device pointers; each output
+ *                   column must hold n_tokens elements (the upper bound, so no
+ *                   host sync is needed to size it). 16-byte aligned columns
+ *                   take the vector path.
+ * elem_bytes        [host] int32 [n_cols]
+ * offsets_out       int64 [n_traj+1]: entries 0..n_kept hold the packed CSR
+ * kept_ids_out      int32 [n_traj]:   entries 0..n_kept-1 hold the kept ids
+ * n_kept_tokens_out int64 [1] device scalar: offsets_out[n_kept] */
+int pace_compact(const int64_t *offsets, int64_t n_traj, int64_t n_tokens, const uint8_t *keep,
+                 int n_cols, const void *const *cols_in, const int32_t *elem_bytes,
+                 void *const *cols_out, int64_t *offsets_out, int32_t *kept_ids_out,
+                 int64_t *n_kept_tokens_out, void *workspace, size_t workspace_bytes,
+                 void *stream);
+
+/* pace_validate -- device check of the data preconditions of Lemma 1
+ * (v_t <= c(tau) <= j) and of the CSR layout. Writes the OR of the
+ * PACE_BAD_* bits that apply to *err_word_out (int32 device scalar; 0 = all
+ * preconditions hold). window_sorted may be NULL (window_n = 0). */
+int pace_validate(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                  const int32_t *completion, int32_t current_version,
+                  const double *window_sorted, int64_t window_n, int32_t *err_word_out,
+                  void *stream);
+
+/* Static description of an error code. */
+const char *pace_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PACE_H */

@@ -1,0 +1,243 @@
+"""PACE pool filter step on AMD Instinct MI355X (gfx950).
+
+Thin ctypes binding of ``libpace.so`` (declared in ``include/pace.h``). Each
+function has the C entry point's name and only marshals arguments: it checks
+tensor dtypes/devices, allocates output tensors that were not supplied, and
+passes raw device pointers plus the current HIP stream. Every step of the
+filter runs in the library's HIP kernels; there is no CPU or PyTorch
+fallback, and importing this package on a machine without the built library
+fails loudly.
+
+    score, S, T      = pace_score(tags, offsets, completion, V, prefix, window)
+    budget, r_hat    = pace_budget(occupancy, capacity, r_hat_prev=0.0)
+    keep, reject_ids = pace_select(score, budget)
+    off_out, ids, n_kept_tokens, packed = pace_compact(offsets, keep, [tags])
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional, Sequence
+
+import torch
+
+from ._lib import PaceParams, lib, library_path
+
+__all__ = [
+    "PaceError", "PaceParams", "default_params", "pace_workspace_bytes", "pace_score",
+    "pace_budget", "pace_select", "pace_compact", "pace_validate", "FilterStep",
+    "library_path", "WS_SCORE", "WS_SELECT", "WS_COMPACT",
+    "BAD_OFFSETS", "BAD_COMPLETION", "BAD_TAG", "BAD_WINDOW",
+]
+
+WS_SCORE, WS_SELECT, WS_COMPACT = 0, 1, 2
+BAD_OFFSETS, BAD_COMPLETION, BAD_TAG, BAD_WINDOW = 0x1, 0x2, 0x4, 0x8
+
+
+class PaceError(RuntimeError):
+    def __init__(self, code: int, fn: str):
+        msg = lib().pace_strerror(code).decode()
+        super().__init__("%s: %s (code %d)" % (fn, msg, code))
+        self.code = code
+
+
+def _check(code: int, fn: str):
+    if code != 0:
+        raise PaceError(code, fn)
+
+
+def default_params(**kw) -> PaceParams:
+    p = PaceParams()
+    lib().pace_default_params(ctypes.byref(p))
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dev(t: torch.Tensor, dtype, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if t.dtype != dtype:
+        raise ValueError("%s must have dtype %s, got %s" % (name, dtype, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return t
+
+
+def _stream(device: torch.device, stream=None) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def pace_workspace_bytes(which: int, n_traj: int, n_tokens: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().pace_workspace_bytes(int(which), int(n_traj), int(n_tokens), ctypes.byref(out)),
+           "pace_workspace_bytes")
+    return int(out.value)
+
+
+def _workspace(which, n, nt, device, ws):
+    need = pace_workspace_bytes(which, n, nt)
+    if ws is None:
+        ws = torch.empty(max(need, 256), dtype=torch.uint8, device=device)
+    return ws
+
+
+def pace_score(tags, offsets, completion, current_version, prefix_score=None, window_sorted=None,
+               params: Optional[PaceParams] = None, score_out=None, gen_sum_out=None,
+               gen_count_out=None, workspace=None, stream=None, with_counts=True):
+    """Eq. (1)-(2), (6)-(9). Returns (score f64[n], S i64[n] or None, T i64[n] or None)."""
+    _dev(tags, torch.int32, "tags")
+    _dev(offsets, torch.int64, "offsets")
+    _dev(completion, torch.int32, "completion")
+    n = offsets.numel() - 1
+    nt = tags.numel()
+    dev = tags.device
+    if prefix_score is not None:
+        _dev(prefix_score, torch.float64, "prefix_score")
+    W = 0
+    if window_sorted is not None:
+        _dev(window_sorted, torch.float64, "window_sorted")
+        W = window_sorted.numel()
+    if score_out is None:
+        score_out = torch.empty(n, dtype=torch.float64, device=dev)
+    if with_counts:
+        if gen_sum_out is None:
+            gen_sum_out = torch.empty(n, dtype=torch.int64, device=dev)
+        if gen_count_out is None:
+            gen_count_out = torch.empty(n, dtype=torch.int64, device=dev)
+    ws = _workspace(WS_SCORE, n, nt, dev, workspace)
+    _check(lib().pace_score(_ptr(tags), _ptr(offsets), n, nt, _ptr(completion), int(current_version),
+                            _ptr(prefix_score), _ptr(window_sorted), W,
+                            ctypes.byref(params) if params is not None else None,
+                            _ptr(score_out), _ptr(gen_sum_out), _ptr(gen_count_out),
+                            _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_score")
+    return score_out, gen_sum_out, gen_count_out
+
+
+def pace_budget(occupancy: int, capacity: int, params: Optional[PaceParams] = None,
+                r_hat_prev: float = 0.0):
+    """Eq. (3)-(4) on the host. Returns (budget, r_hat)."""
+    rh = ctypes.c_double(float(r_hat_prev))
+    b = ctypes.c_int64(0)
+    _check(lib().pace_budget(int(occupancy), int(capacity),
+                             ctypes.byref(params) if params is not None else None,
+                             ctypes.byref(rh), ctypes.byref(b)), "pace_budget")
+    return int(b.value), float(rh.value)
+
+
+def pace_select(score, budget: int, keep_out=None, reject_ids_out=None, workspace=None, stream=None):
+    """Reject exactly `budget` highest scores, ties to the lower id.
+    Returns (keep u8[n], reject_ids i32[budget])."""
+    _dev(score, torch.float64, "score")
+    n = score.numel()
+    dev = score.device
+    if keep_out is None:
+        keep_out = torch.empty(n, dtype=torch.uint8, device=dev)
+    if reject_ids_out is None:
+        reject_ids_out = torch.empty(max(int(budget), 1), dtype=torch.int32, device=dev)
+    ws = _workspace(WS_SELECT, n, 0, dev, workspace)
+    _check(lib().pace_select(_ptr(score), n, int(budget), _ptr(keep_out), _ptr(reject_ids_out),
+                             _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_select")
+    return keep_out, reject_ids_out[: int(budget)]
+
+
+def pace_compact(offsets, keep, cols: Sequence[torch.Tensor], cols_out=None, offsets_out=None,
+                 kept_ids_out=None, n_kept_tokens_out=None, workspace=None, stream=None,
+                 n_tokens: Optional[int] = None):
+    """Pack kept spans of every column. Returns (offsets_out i64[n+1], kept_ids i32[n],
+    n_kept_tokens i64[1] device scalar, packed columns at full capacity). Only the
+    first n_kept+1 / n_kept / n_kept_tokens entries are meaningful."""
+    _dev(offsets, torch.int64, "offsets")
+    _dev(keep, torch.uint8, "keep")
+    n = offsets.numel() - 1
+    dev = offsets.device
+    cols = list(cols)
+    if n_tokens is None:
+        n_tokens = cols[0].numel() if cols else int(offsets[-1].item())
+    for k, c in enumerate(cols):
+        if not c.is_cuda or not c.is_contiguous() or c.numel() != n_tokens:
+            raise ValueError("column %d must be a contiguous device tensor of n_tokens elements" % k)
+    if cols_out is None:
+        cols_out = [torch.empty_like(c) for c in cols]
+    if offsets_out is None:
+        offsets_out = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    if kept_ids_out is None:
+        kept_ids_out = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+    if n_kept_tokens_out is None:
+        n_kept_tokens_out = torch.empty(1, dtype=torch.int64, device=dev)
+    ws = _workspace(WS_COMPACT, n, n_tokens, dev, workspace)
+    nc = len(cols)
+    cin = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols])
+    cout = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols_out])
+    eb = (ctypes.c_int32 * max(nc, 1))(*[c.element_size() for c in cols])
+    _check(lib().pace_compact(_ptr(offsets), n, int(n_tokens), _ptr(keep), nc, cin, eb, cout,
+                              _ptr(offsets_out), _ptr(kept_ids_out), _ptr(n_kept_tokens_out),
+                              _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_compact")
+    return offsets_out, kept_ids_out, n_kept_tokens_out, cols_out
+
+
+def pace_validate(tags, offsets, completion, current_version, window_sorted=None, err_out=None,
+                  stream=None):
+    """Device check of Lemma 1's preconditions. Returns the int32[1] error word tensor."""
+    _dev(tags, torch.int32, "tags")
+    _dev(offsets, torch.int64, "offsets")
+    _dev(completion, torch.int32, "completion")
+    dev = tags.device
+    W = 0
+    if window_sorted is not None:
+        _dev(window_sorted, torch.float64, "window_sorted")
+        W = window_sorted.numel()
+    if err_out is None:
+        err_out = torch.empty(1, dtype=torch.int32, device=dev)
+    _check(lib().pace_validate(_ptr(tags), _ptr(offsets), offsets.numel() - 1, tags.numel(),
+                               _ptr(completion), int(current_version), _ptr(window_sorted), W,
+                               _ptr(err_out), _stream(dev, stream)), "pace_validate")
+    return err_out
+
+
+class FilterStep:
+    """Preallocated buffers for repeated filter steps over pools of one shape
+    (n trajectories, n_tokens tokens, the given payload columns). ``run``
+    enqueues score -> budget -> select -> compact on the current stream with no
+    allocation and no host synchronisation."""
+
+    def __init__(self, n: int, n_tokens: int, col_dtypes: Sequence[torch.dtype], device,
+                 params: Optional[PaceParams] = None):
+        dev = torch.device(device)
+        self.n, self.n_tokens, self.device = n, n_tokens, dev
+        self.params = params if params is not None else default_params()
+        e = lambda k, dt: torch.empty(k, dtype=dt, device=dev)
+        self.score = e(max(n, 1), torch.float64)
+        self.gen_sum = e(max(n, 1), torch.int64)
+        self.gen_count = e(max(n, 1), torch.int64)
+        self.keep = e(max(n, 1), torch.uint8)
+        self.reject_ids = e(max(n, 1), torch.int32)
+        self.offsets_out = e(n + 1, torch.int64)
+        self.kept_ids = e(max(n, 1), torch.int32)
+        self.n_kept_tokens = e(1, torch.int64)
+        self.cols_out = [e(max(n_tokens, 1), dt) for dt in col_dtypes]
+        self.ws = [e(max(pace_workspace_bytes(w, n, n_tokens), 256), torch.uint8)
+                   for w in (WS_SCORE, WS_SELECT, WS_COMPACT)]
+        self.r_hat = 0.0
+        self.budget = 0
+
+    def score_only(self, tags, offsets, completion, V, prefix=None, window=None, stream=None):
+        return pace_score(tags, offsets, completion, V, prefix, window, self.params,
+                          self.score[: self.n], self.gen_sum[: self.n], self.gen_count[: self.n],
+                          self.ws[0], stream)
+
+    def run(self, tags, offsets, completion, V, occupancy, capacity, cols, prefix=None,
+            window=None, stream=None):
+        self.score_only(tags, offsets, completion, V, prefix, window, stream)
+        self.budget, self.r_hat = pace_budget(occupancy, capacity, self.params, self.r_hat)
+        pace_select(self.score[: self.n], self.budget, self.keep[: self.n], self.reject_ids,
+                    self.ws[1], stream)
+        pace_compact(offsets, self.keep[: self.n], cols, [c[: self.n_tokens] for c in self.cols_out],
+                     self.offsets_out, self.kept_ids, self.n_kept_tokens, self.ws[2], stream,
+                     n_tokens=self.n_tokens)
+        return self

@@ -1,0 +1,194 @@
+// C ABI of the PACE filter step (declared in include/pace.h): host-side
+// argument checks, workspace carving and kernel launches. All device work is
+// enqueued on the caller's stream; nothing here allocates or synchronises.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <hip/hip_runtime_api.h>
+
+#include "../../include/pace.h"
+#include "kernels.hpp"
+
+#pragma clang fp contract(off)
+
+using namespace pace;
+
+namespace {
+
+bool aligned(const void *p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+pace_params params_or_default(const pace_params *p) {
+    pace_params d;
+    pace_default_params(&d);
+    return p ? *p : d;
+}
+
+int64_t ipow_checked(int64_t x, int g, bool *overflow) {
+    // x^g for the 2^53 check of the prefix window; saturates on overflow
+    int64_t r = 1;
+    for (int k = 0; k < g; ++k) {
+        if (x != 0 && r > INT64_MAX / x) {
+            *overflow = true;
+            return INT64_MAX;
+        }
+        r *= x;
+    }
+    return r;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? PACE_OK : PACE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+void pace_default_params(pace_params *p) {
+    if (!p) return;
+    p->w_wait = 1.0;
+    p->gamma = 4;
+    p->window_min = 32;
+    p->beta = 0.0;
+    p->r_max = 0.9;
+}
+
+const char *pace_strerror(int code) {
+    switch (code) {
+        case PACE_OK: return "ok";
+        case PACE_ERR_INVALID_ARG: return "invalid argument";
+        case PACE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+        case PACE_ERR_PRECONDITION: return "data precondition violated";
+        case PACE_ERR_HIP: return "HIP launch failure";
+        default: return "unknown error code";
+    }
+}
+
+int pace_workspace_bytes(int which, int64_t n_traj, int64_t n_tokens, size_t *bytes_out) {
+    if (!bytes_out || n_traj < 0 || n_tokens < 0) return PACE_ERR_INVALID_ARG;
+    switch (which) {
+        case PACE_WS_SCORE: *bytes_out = score_ws_bytes(n_traj, n_tokens); return PACE_OK;
+        case PACE_WS_SELECT: *bytes_out = select_ws_bytes(n_traj); return PACE_OK;
+        case PACE_WS_COMPACT: *bytes_out = compact_ws_bytes(n_traj, n_tokens); return PACE_OK;
+        default: return PACE_ERR_INVALID_ARG;
+    }
+}
+
+int pace_score(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+               const int32_t *completion, int32_t current_version, const double *prefix_score,
+               const double *window_sorted, int64_t window_n, const pace_params *params,
+               double *score_out, int64_t *gen_sum_out, int64_t *gen_count_out, void *workspace,
+               size_t workspace_bytes, void *stream) {
+    const pace_params p = params_or_default(params);
+    if (n_traj < 0 || n_traj >= INT32_MAX || n_tokens < 0 || window_n < 0) return PACE_ERR_INVALID_ARG;
+    if (!offsets || (n_traj > 0 && (!completion || !score_out)) || (n_tokens > 0 && !tags))
+        return PACE_ERR_INVALID_ARG;
+    if (!aligned(tags, 4) || !aligned(offsets, 8) || !aligned(completion, 4) ||
+        !aligned(score_out, 8) || !aligned(gen_sum_out, 8) || !aligned(gen_count_out, 8) ||
+        !aligned(prefix_score, 8) || !aligned(window_sorted, 8))
+        return PACE_ERR_INVALID_ARG;
+    if (current_version < 0 || current_version == INT32_MAX) return PACE_ERR_INVALID_ARG;
+    if (!(p.w_wait >= 0.0) || isinf(p.w_wait) || p.gamma < 1 || p.gamma > 4 || p.window_min < 0)
+        return PACE_ERR_INVALID_ARG;
+    if (window_n > 0 && !window_sorted) return PACE_ERR_INVALID_ARG;
+    bool of = false;
+    if (window_n > 0 && (ipow_checked(window_n, p.gamma, &of) >= ((int64_t)1 << 53) || of))
+        return PACE_ERR_INVALID_ARG;
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < score_ws_bytes(n_traj, n_tokens))
+        return PACE_ERR_WORKSPACE;
+    const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
+    const bool use_prefix = prefix_score != nullptr && window_n >= wmin;
+    const ScoreWorkspace ws = score_ws_carve(workspace, n_traj, n_tokens);
+    return hip_status(launch_score(tags, offsets, n_traj, n_tokens, completion, current_version,
+                                   prefix_score, window_sorted, window_n, use_prefix, p.w_wait,
+                                   p.gamma, score_out, gen_sum_out, gen_count_out, ws,
+                                   aligned(tags, 16), (hipStream_t)stream));
+}
+
+int pace_budget(int64_t occupancy, int64_t capacity, const pace_params *params,
+                double *r_hat_inout, int64_t *budget_out) {
+    const pace_params p = params_or_default(params);
+    if (!r_hat_inout || !budget_out || occupancy < 0 || capacity < 0) return PACE_ERR_INVALID_ARG;
+    if (!(p.beta >= 0.0 && p.beta < 1.0) || !(p.r_max >= 0.0 && p.r_max <= 1.0))
+        return PACE_ERR_INVALID_ARG;
+    const double prev = *r_hat_inout;
+    if (!(prev >= 0.0) || isinf(prev)) return PACE_ERR_INVALID_ARG;
+    // Eq. (3): fraction of the pool above the target occupancy, clipped.
+    const double surplus_frac = (double)(occupancy - capacity) / (double)(occupancy > 1 ? occupancy : 1);
+    const double r = surplus_frac < 0.0 ? 0.0 : (surplus_frac > 1.0 ? 1.0 : surplus_frac);
+    // Eq. (4): exponential smoothing (two products then one sum, never fused).
+    const double kept_part = p.beta * prev;
+    const double new_part = (1.0 - p.beta) * r;
+    const double r_hat = kept_part + new_part;
+    int64_t b = 0;
+    if (occupancy > capacity) {
+        const double capped = r_hat < p.r_max ? r_hat : p.r_max;
+        b = (int64_t)nearbyint(capped * (double)occupancy);   // ties to even
+        const int64_t surplus = occupancy - capacity;
+        if (b > surplus) b = surplus;
+        if (b < 0) b = 0;
+    }
+    *r_hat_inout = r_hat;
+    *budget_out = b;
+    return PACE_OK;
+}
+
+int pace_select(const double *score, int64_t n_traj, int64_t budget, uint8_t *keep_out,
+                int32_t *reject_ids_out, void *workspace, size_t workspace_bytes, void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || budget < 0 || budget > n_traj) return PACE_ERR_INVALID_ARG;
+    if (n_traj > 0 && (!score || !keep_out)) return PACE_ERR_INVALID_ARG;
+    if (budget > 0 && !reject_ids_out) return PACE_ERR_INVALID_ARG;
+    if (!aligned(score, 8) || !aligned(reject_ids_out, 4)) return PACE_ERR_INVALID_ARG;
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < select_ws_bytes(n_traj))
+        return PACE_ERR_WORKSPACE;
+    return hip_status(launch_select(score, n_traj, budget, keep_out, reject_ids_out, workspace,
+                                    (hipStream_t)stream));
+}
+
+int pace_compact(const int64_t *offsets, int64_t n_traj, int64_t n_tokens, const uint8_t *keep,
+                 int n_cols, const void *const *cols_in, const int32_t *elem_bytes,
+                 void *const *cols_out, int64_t *offsets_out, int32_t *kept_ids_out,
+                 int64_t *n_kept_tokens_out, void *workspace, size_t workspace_bytes,
+                 void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || n_tokens < 0 || n_cols < 0 || n_cols > kMaxCols)
+        return PACE_ERR_INVALID_ARG;
+    if (!offsets || !offsets_out || !n_kept_tokens_out || (n_traj > 0 && (!keep || !kept_ids_out)))
+        return PACE_ERR_INVALID_ARG;
+    if (!aligned(offsets, 8) || !aligned(offsets_out, 8) || !aligned(n_kept_tokens_out, 8) ||
+        !aligned(kept_ids_out, 4))
+        return PACE_ERR_INVALID_ARG;
+    if (n_cols > 0 && (!cols_in || !cols_out || !elem_bytes)) return PACE_ERR_INVALID_ARG;
+    CompactCols cols;
+    memset(&cols, 0, sizeof(cols));
+    for (int c = 0; c < n_cols; ++c) {
+        const int32_t e = elem_bytes[c];
+        if (!(e == 1 || e == 2 || e == 4 || e == 8)) return PACE_ERR_INVALID_ARG;
+        if (n_tokens > 0 && (!cols_in[c] || !cols_out[c])) return PACE_ERR_INVALID_ARG;
+        if (!aligned(cols_in[c], (uintptr_t)e) || !aligned(cols_out[c], (uintptr_t)e))
+            return PACE_ERR_INVALID_ARG;
+        if (n_tokens > INT64_MAX / 8) return PACE_ERR_INVALID_ARG;
+        cols.in[c] = cols_in[c];
+        cols.out[c] = cols_out[c];
+        cols.elem[c] = e;
+        cols.vec[c] = (aligned(cols_in[c], 16) && aligned(cols_out[c], 16)) ? 1 : 0;
+    }
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < compact_ws_bytes(n_traj, n_tokens))
+        return PACE_ERR_WORKSPACE;
+    return hip_status(launch_compact(offsets, n_traj, n_tokens, keep, cols, n_cols, offsets_out,
+                                     kept_ids_out, n_kept_tokens_out, workspace, (hipStream_t)stream));
+}
+
+int pace_validate(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                  const int32_t *completion, int32_t current_version, const double *window_sorted,
+                  int64_t window_n, int32_t *err_word_out, void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || n_tokens < 0 || window_n < 0) return PACE_ERR_INVALID_ARG;
+    if (!offsets || !err_word_out || (n_traj > 0 && !completion) || (n_tokens > 0 && !tags) ||
+        (window_n > 0 && !window_sorted))
+        return PACE_ERR_INVALID_ARG;
+    if (!aligned(tags, 4) || !aligned(offsets, 8) || !aligned(completion, 4) ||
+        !aligned(err_word_out, 4) || !aligned(window_sorted, 8))
+        return PACE_ERR_INVALID_ARG;
+    return hip_status(launch_validate(tags, offsets, n_traj, n_tokens, completion, current_version,
+                                      window_sorted, window_n, err_word_out, (hipStream_t)stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,304 @@
+// pace_score kernels for gfx950.
+//
+// Step 1 (score_reduce): every per-token version tag is read exactly once.
+// The token array is cut into chunks of kScoreChunk tokens, one chunk per
+// wave64; a chunk is read as 16-byte vectors, 8 per lane in flight. The wave
+// walks the trajectory boundaries that fall inside its chunk and keeps, per
+// lane, the running piece sum of (tag + 1) over generated tokens (masked
+// tags, -1, add 0) and the generated-token count. When a trajectory ends the
+// wave reduces the piece across lanes and lane 0 stores it:
+//   - the piece of a trajectory that starts inside this chunk goes to
+//     part_{sum,cnt}[trajectory] (exactly one chunk holds each start);
+//   - the piece of the trajectory that straddles the chunk start goes to
+//     carry_{sum,cnt}[chunk] (at most one per chunk).
+// No atomics, no zero-filled workspace, and the combine order is fixed, so
+// the integer results are bit-identical run to run.
+//
+// Step 2 (score_finalize): one thread per trajectory adds its carries, forms
+// S_i = c_i T_i - sum(tag) exactly in int64 and evaluates the score of
+// Eq. (6)-(9) in binary64 with a fixed operation order (no contraction).
+#include "device_util.hpp"
+#include "kernels.hpp"
+
+#pragma clang fp contract(off)
+
+namespace pace {
+
+namespace {
+
+constexpr int kVec = 4;                       // tags per lane per window
+constexpr int kWin = kWave * kVec;            // 256 tokens per wave window
+constexpr int kUnroll = 8;                    // windows in flight per wave
+constexpr int kSuper = kWin * kUnroll;        // 2048
+constexpr int kWavesPerBlock = 4;
+static_assert(kScoreChunk % kSuper == 0, "chunk must be a multiple of the super-window");
+
+// Lane k caches clamp(off[base + k], 0, NT); reads of increasing indices only.
+struct BoundCache {
+    int64_t base;
+    int64_t val;
+    __device__ __forceinline__ void load(const int64_t *__restrict__ off, int64_t n, int64_t NT, int64_t b) {
+        base = b;
+        int64_t idx = b + lane_id();
+        val = (idx <= n) ? clamp64(off[idx], 0, NT) : NT;
+    }
+    __device__ __forceinline__ int64_t get(const int64_t *__restrict__ off, int64_t n, int64_t NT, int64_t i) {
+        if (i < base || i - base >= kWave) load(off, n, NT, i);
+        return readlane_i64(val, (int)(i - base));
+    }
+};
+
+__device__ __forceinline__ void add_all(const int4 &v, uint32_t &s, uint32_t &c) {
+    uint32_t u0 = (uint32_t)v.x + 1u, u1 = (uint32_t)v.y + 1u;
+    uint32_t u2 = (uint32_t)v.z + 1u, u3 = (uint32_t)v.w + 1u;
+    s += u0 + u1 + u2 + u3;
+    c += (u0 != 0u) + (u1 != 0u) + (u2 != 0u) + (u3 != 0u);
+}
+
+__device__ __forceinline__ void add_all_wide(const int4 &v, uint64_t &s, uint32_t &c) {
+    uint32_t u0 = (uint32_t)v.x + 1u, u1 = (uint32_t)v.y + 1u;
+    uint32_t u2 = (uint32_t)v.z + 1u, u3 = (uint32_t)v.w + 1u;
+    s += (uint64_t)u0 + (uint64_t)u1 + (uint64_t)u2 + (uint64_t)u3;
+    c += (u0 != 0u) + (u1 != 0u) + (u2 != 0u) + (u3 != 0u);
+}
+
+// Elements of this lane's vector whose positions lie in [lo, hi).
+__device__ __forceinline__ void add_range(const int4 &v, int64_t p0, int64_t lo, int64_t hi,
+                                          uint64_t &s, uint32_t &c) {
+    const int x[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        int64_t p = p0 + e;
+        if (p >= lo && p < hi) {
+            uint32_t u = (uint32_t)x[e] + 1u;
+            s += u;
+            c += (u != 0u);
+        }
+    }
+}
+
+// kNarrow: every tag + 1 < 2^24, so a lane's 32 tags of one super-window sum
+// below 2^29 in 32 bits before widening.
+template <bool kNarrow, bool kVecLoad>
+__global__ __launch_bounds__(256) void score_reduce_kernel(
+    const int32_t *__restrict__ tags, const int64_t *__restrict__ off, int64_t n, int64_t NT,
+    int64_t n_chunks, uint64_t *__restrict__ part_sum, int64_t *__restrict__ part_cnt,
+    uint64_t *__restrict__ carry_sum, int64_t *__restrict__ carry_cnt) {
+    const int lane = lane_id();
+    const int64_t chunk = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x / kWave);
+    if (chunk >= n_chunks) return;
+    const int64_t cs = chunk * kScoreChunk;
+    const int64_t ce = (cs + kScoreChunk < NT) ? cs + kScoreChunk : NT;
+
+    // Trajectory that contains the chunk's first token.
+    const int64_t s = wave_last_le(off, n, cs);
+    BoundCache bc;
+    int64_t cur, cur_end;
+    bool valid = false, pending = false, carry_piece = false;
+    if (s < 0) {                 // only for malformed offsets: tokens before offsets[0]
+        cur = -1;
+        bc.load(off, n, NT, 0);
+        cur_end = readlane_i64(bc.val, 0);
+    } else if (s >= n) {         // tokens at or past offsets[n]
+        cur = n;
+        bc.load(off, n, NT, n);
+        cur_end = INT64_MAX;
+    } else {
+        cur = s;
+        bc.load(off, n, NT, s);
+        const int64_t cur_start = readlane_i64(bc.val, 0);
+        cur_end = bc.get(off, n, NT, s + 1);
+        valid = true;
+        pending = true;
+        carry_piece = cur_start < cs;
+    }
+
+    uint64_t acc_s = 0;
+    uint32_t acc_c = 0;
+
+    auto flush = [&]() {
+        const uint64_t ts = wave_sum_u64(acc_s);
+        const uint64_t tc = wave_sum_u64((uint64_t)acc_c);
+        if (lane == 0) {
+            if (carry_piece) {
+                carry_sum[chunk] = ts;
+                carry_cnt[chunk] = (int64_t)tc;
+            } else {
+                part_sum[cur] = ts;
+                part_cnt[cur] = (int64_t)tc;
+            }
+        }
+        acc_s = 0;
+        acc_c = 0;
+    };
+
+    for (int64_t pos = cs; pos < ce; pos += kSuper) {
+        int4 v[kUnroll];
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int64_t q = pos + (int64_t)k * kWin + (int64_t)lane * kVec;
+            if (kVecLoad && q + kVec <= ce) {
+                v[k] = *reinterpret_cast<const int4 *>(tags + q);
+            } else {
+                v[k] = make_int4(-1, -1, -1, -1);
+                if (q < ce) v[k].x = tags[q];
+                if (q + 1 < ce) v[k].y = tags[q + 1];
+                if (q + 2 < ce) v[k].z = tags[q + 2];
+                if (q + 3 < ce) v[k].w = tags[q + 3];
+            }
+        }
+        const int64_t send = (pos + kSuper < ce) ? pos + kSuper : ce;
+        if (valid && cur_end >= send) {
+            // Fast path: the whole super-window lies in trajectory `cur`.
+            if (kNarrow) {
+                uint32_t s32 = 0, c32 = 0;
+#pragma unroll
+                for (int k = 0; k < kUnroll; ++k) add_all(v[k], s32, c32);
+                acc_s += s32;
+                acc_c += c32;
+            } else {
+#pragma unroll
+                for (int k = 0; k < kUnroll; ++k) add_all_wide(v[k], acc_s, acc_c);
+            }
+            continue;
+        }
+        // Boundary path: walk trajectory ends window by window.
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) {
+            const int64_t w = pos + (int64_t)k * kWin;
+            if (w >= ce) break;
+            const int64_t we = (w + kWin < ce) ? w + kWin : ce;
+            const int64_t p0 = w + (int64_t)lane * kVec;
+            int64_t lo = w;
+            while (true) {
+                const int64_t hi = cur_end < we ? cur_end : we;
+                if (valid && hi > lo) add_range(v[k], p0, lo, hi, acc_s, acc_c);
+                if (cur_end > we) break;          // trajectory continues past this window
+                if (pending) flush();             // trajectory `cur` ends at cur_end
+                lo = cur_end;
+                ++cur;
+                while (cur < n && bc.get(off, n, NT, cur + 1) <= lo) ++cur;   // skip empty ones
+                carry_piece = false;
+                if (cur >= n) {
+                    valid = false;
+                    pending = false;
+                    cur_end = INT64_MAX;
+                } else {
+                    valid = true;
+                    cur_end = bc.get(off, n, NT, cur + 1);
+                    pending = lo < ce;
+                }
+                if (lo >= we) break;
+            }
+        }
+    }
+    if (pending) flush();
+}
+
+template <bool kWinLds>
+__global__ __launch_bounds__(256) void score_finalize_kernel(
+    const int64_t *__restrict__ off, int64_t n, int64_t NT, const int32_t *__restrict__ completion,
+    int32_t V, const double *__restrict__ prefix, const double *__restrict__ window, int64_t W,
+    int use_prefix, double w_wait, int gamma, const uint64_t *__restrict__ part_sum,
+    const int64_t *__restrict__ part_cnt, const uint64_t *__restrict__ carry_sum,
+    const int64_t *__restrict__ carry_cnt, double *__restrict__ score,
+    int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count) {
+    __shared__ double win_lds[kWinLds ? kWindowLdsMax : 1];
+    if (kWinLds && use_prefix) {
+        for (int64_t k = threadIdx.x; k < W; k += blockDim.x) win_lds[k] = window[k];
+        __syncthreads();
+    }
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+
+    const int64_t lo = clamp64(off[i], 0, NT), hi = clamp64(off[i + 1], 0, NT);
+    uint64_t sp = 0;
+    int64_t T = 0;
+    if (hi > lo) {
+        sp = part_sum[i];
+        T = part_cnt[i];
+        for (int64_t c = lo / kScoreChunk + 1; c * kScoreChunk < hi; ++c) {
+            sp += carry_sum[c];
+            T += carry_cnt[c];
+        }
+    }
+    const int64_t c = completion[i];
+    // sp = sum(tag) + T over generated tokens; S = sum(c - tag) = c T - sum(tag).
+    const int64_t sum_tag = (int64_t)(sp - (uint64_t)T);
+    const int64_t S = c * T - sum_tag;
+
+    const double k_wait = (double)((int64_t)V - c);
+    const double k_gen = (T > 0) ? (double)S / (double)T : 0.0;
+    double F = 1.0;
+    if (use_prefix) {
+        const double sv = prefix[i];
+        if (!__builtin_isnan(sv)) {
+            int64_t a_lo = 0, a_hi = W;        // count of window entries <= sv
+            while (a_lo < a_hi) {
+                const int64_t mid = (a_lo + a_hi) >> 1;
+                const double wv = kWinLds ? win_lds[mid] : window[mid];
+                if (wv <= sv) a_lo = mid + 1; else a_hi = mid;
+            }
+            int64_t A = 1, B = 1;
+            for (int g = 0; g < gamma; ++g) {
+                A *= a_lo;
+                B *= (W - a_lo);
+            }
+            F = (double)A / (double)(A + B);
+        }
+    }
+    const double wait_term = w_wait * k_wait;
+    const double gen_term = F * k_gen;
+    score[i] = wait_term + gen_term;
+    if (gen_sum) gen_sum[i] = S;
+    if (gen_count) gen_count[i] = T;
+}
+
+}  // namespace
+
+size_t score_ws_bytes(int64_t n, int64_t n_tokens) {
+    const int64_t ch = score_chunks(n_tokens);
+    return align256((size_t)n * 8) * 2 + align256((size_t)ch * 8) * 2 + 256;
+}
+
+ScoreWorkspace score_ws_carve(void *ws, int64_t n, int64_t n_tokens) {
+    const int64_t ch = score_chunks(n_tokens);
+    char *p = (char *)ws;
+    ScoreWorkspace w;
+    w.part_sum = (uint64_t *)p;  p += align256((size_t)n * 8);
+    w.part_cnt = (int64_t *)p;   p += align256((size_t)n * 8);
+    w.carry_sum = (uint64_t *)p; p += align256((size_t)ch * 8);
+    w.carry_cnt = (int64_t *)p;
+    return w;
+}
+
+hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                        const int32_t *completion, int32_t V, const double *prefix,
+                        const double *window, int64_t W, bool use_prefix, double w_wait, int gamma,
+                        double *score, int64_t *gen_sum, int64_t *gen_count,
+                        const ScoreWorkspace &ws, bool vec_ok, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const int64_t ch = score_chunks(n_tokens);
+    if (ch > 0) {
+        const unsigned grid = (unsigned)((ch + kWavesPerBlock - 1) / kWavesPerBlock);
+        const bool narrow = (int64_t)V < (1 << 24) - 1;
+        if (narrow && vec_ok)
+            score_reduce_kernel<true, true><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
+        else if (narrow)
+            score_reduce_kernel<true, false><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
+        else if (vec_ok)
+            score_reduce_kernel<false, true><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
+        else
+            score_reduce_kernel<false, false><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const unsigned grid = (unsigned)((n + 255) / 256);
+    if (use_prefix && W <= kWindowLdsMax)
+        score_finalize_kernel<true><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt, score, gen_sum, gen_count);
+    else
+        score_finalize_kernel<false><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt, score, gen_sum, gen_count);
+    return hipGetLastError();
+}
+
+}  // namespace pace

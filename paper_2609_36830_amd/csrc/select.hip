@@ -1,0 +1,188 @@
+// pace_select kernel for gfx950: reject exactly `budget` trajectories, the
+// first ones in the order (score descending, id ascending) -- the quantile
+// rejection rule of Sec. 3.1 taken over the current pool with an exact count.
+//
+// One workgroup of 1024 threads (16 waves). Each score becomes a 64-bit key
+// whose unsigned order is the score order (sign-magnitude flip; -0 -> +0).
+// An MSB-first radix select with 8-bit digits finds the budget-th largest
+// key K: each pass histograms the digit of the keys still tied with the
+// prefix found so far (LDS atomics), and a 256-bin suffix scan over four
+// waves picks the digit bin that holds the cut. The search stops early when
+// the cut falls exactly on a bin boundary. Keys above K are rejected; among
+// keys equal to K the lowest ids are rejected, found with a block-wide
+// ordered count (ballot + popcount per wave). Rejected ids are written in
+// ascending order by a second ordered count.
+#include "device_util.hpp"
+#include "kernels.hpp"
+
+namespace pace {
+
+namespace {
+
+constexpr int kT = kSelectThreads;
+constexpr int kNW = kT / kWave;   // 16 waves
+
+__device__ __forceinline__ uint64_t score_key(double d) {
+    if (__builtin_isnan(d)) return ~0ull;    // precondition violation: above +inf
+    if (d == 0.0) d = 0.0;                    // -0 and +0 are the same score
+    const uint64_t b = (uint64_t)__double_as_longlong(d);
+    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
+}
+
+// Exclusive count of `f` over the block in thread order; *total = block sum.
+__device__ __forceinline__ uint32_t block_excl_count(bool f, uint32_t &total, uint32_t *wsum) {
+    const uint64_t m = ballot(f);
+    const uint32_t in_wave = (uint32_t)__popcll(m & lanes_below());
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == 0) wsum[w] = (uint32_t)__popcll(m);
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < kNW; ++k) {
+        const uint32_t x = wsum[k];
+        tot += x;
+        before += (k < w) ? x : 0u;
+    }
+    __syncthreads();
+    total = tot;
+    return before + in_wave;
+}
+
+// kItems > 0: each thread holds kItems keys in registers (n <= 1024*kItems).
+// kItems == 0: keys staged in the workspace (any n < 2^31).
+template <int kItems>
+__global__ __launch_bounds__(kT) void select_kernel(const double *__restrict__ score, int64_t n,
+                                                    int64_t budget, uint8_t *__restrict__ keep,
+                                                    int32_t *__restrict__ reject_ids,
+                                                    uint64_t *__restrict__ wkeys) {
+    const int tid = threadIdx.x;
+    const int64_t n_items = kItems ? kItems : (n + kT - 1) / kT;
+    uint64_t kr[kItems ? kItems : 1];
+
+    __shared__ uint32_t hist[256];
+    __shared__ uint32_t wsum[kNW];
+    __shared__ uint32_t sel_digit, sel_before, sel_cnt;
+
+    // Load scores as keys.
+    if (kItems) {
+#pragma unroll
+        for (int it = 0; it < (kItems ? kItems : 1); ++it) {
+            const int64_t i = (int64_t)it * kT + tid;
+            kr[it] = (i < n) ? score_key(score[i]) : 0ull;
+        }
+    } else {
+        for (int64_t it = 0; it < n_items; ++it) {
+            const int64_t i = it * kT + tid;
+            if (i < n) wkeys[i] = score_key(score[i]);
+        }
+    }
+    auto key_at = [&](int64_t it) -> uint64_t {
+        if (kItems) return kr[it];
+        return wkeys[it * kT + tid];
+    };
+
+    // Cut: mode 0 rejects nothing (budget 0), 1 everything (budget n),
+    // 2 every key >= kcut (the cut is a digit-bin boundary), 3 every key > kcut
+    // plus the first need_tie ids whose key equals kcut.
+    int mode = (budget == 0) ? 0 : (budget >= n ? 1 : 3);
+    uint64_t kcut = 0;
+    int64_t need_tie = 0;
+    if (mode == 3) {
+        uint64_t prefix = 0, mask = 0;
+        int64_t need = budget;
+        for (int shift = 56; shift >= 0; shift -= 8) {
+            if (tid < 256) hist[tid] = 0u;
+            __syncthreads();
+#pragma unroll
+            for (int64_t it = 0; it < (kItems ? kItems : n_items); ++it) {
+                const int64_t i = it * kT + tid;
+                if (i < n) {
+                    const uint64_t k = key_at(it);
+                    if (((k ^ prefix) & mask) == 0ull) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+                }
+            }
+            __syncthreads();
+            // Suffix sums over digits 255..0: thread t holds digit 255 - t.
+            uint32_t h = 0, inc = 0;
+            if (tid < 256) {
+                h = hist[255 - tid];
+                inc = wave_incl_scan_u32(h);
+                if (lane_id() == kWave - 1) wsum[tid / kWave] = inc;
+            }
+            __syncthreads();
+            if (tid < 256) {
+                for (int w = 0; w < tid / kWave; ++w) inc += wsum[w];
+                const uint32_t before = inc - h;          // keys with a larger digit
+                if ((int64_t)before < need && (int64_t)inc >= need) {
+                    sel_digit = 255u - (uint32_t)tid;
+                    sel_before = before;
+                    sel_cnt = h;
+                }
+            }
+            __syncthreads();
+            need -= (int64_t)sel_before;
+            prefix |= (uint64_t)sel_digit << shift;
+            mask |= 0xFFull << shift;
+            if (need == (int64_t)sel_cnt) {   // the whole bin is rejected
+                mode = 2;                     // prefix has zero low bits
+                break;
+            }
+        }
+        kcut = prefix;
+        if (mode == 3) need_tie = need;
+    }
+
+    // Classify in id order and emit keep flags and ascending reject ids.
+    int64_t tie_base = 0, rej_base = 0;
+#pragma unroll
+    for (int64_t it = 0; it < n_items; ++it) {
+        const int64_t i = it * kT + tid;
+        const bool in = i < n;
+        const uint64_t k = in ? key_at(it) : 0ull;
+        bool rej;
+        if (mode == 3) {
+            const bool eq = in && (k == kcut);
+            uint32_t tot;
+            const uint32_t r = block_excl_count(eq, tot, wsum);
+            rej = in && ((k > kcut) || (eq && tie_base + (int64_t)r < need_tie));
+            tie_base += tot;
+        } else {
+            rej = in && (mode == 1 || (mode == 2 && k >= kcut));
+        }
+        uint32_t tot2;
+        const uint32_t pos = block_excl_count(rej, tot2, wsum);
+        if (in) {
+            keep[i] = rej ? 0 : 1;
+            if (rej && rej_base + (int64_t)pos < budget) reject_ids[rej_base + pos] = (int32_t)i;
+        }
+        rej_base += tot2;
+    }
+}
+
+}  // namespace
+
+size_t select_ws_bytes(int64_t n) {
+    return (n > (int64_t)kT * kSelectMaxItems) ? align256((size_t)n * 8) : 256;
+}
+
+hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
+                         int32_t *reject_ids, void *ws, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const int64_t items = (n + kT - 1) / kT;
+    uint64_t *wk = (uint64_t *)ws;
+    if (items <= 1)
+        select_kernel<1><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+    else if (items <= 2)
+        select_kernel<2><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+    else if (items <= 4)
+        select_kernel<4><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+    else if (items <= 8)
+        select_kernel<8><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+    else if (items <= 16)
+        select_kernel<16><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+    else
+        select_kernel<0><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+    return hipGetLastError();
+}
+
+}  // namespace pace

@@ -1,0 +1,142 @@
+"""CPU tests of the C ABI: the library loads, exports every entry point that
+include/pace.h declares, and its host-only logic (defaults, workspace sizing,
+the budget of Eq. (3)-(4), host-side argument checks) behaves as documented.
+No GPU call is made here: every argument-error case returns before any
+launch."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pace.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2609_36830_amd import _lib
+    if not os.path.exists(_lib.library_path):
+        from paper_2609_36830_amd import build
+        build.build()
+    return _lib.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:int|void|const char \*)\s*\**\s*(pace_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for f in ("pace_score", "pace_budget", "pace_select", "pace_compact", "pace_validate",
+              "pace_workspace_bytes", "pace_default_params", "pace_strerror"):
+        assert f in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    from paper_2609_36830_amd import _lib
+    names = declared_functions()
+    for f in names:
+        assert hasattr(L, f), f
+    assert sorted(n for n, _, _ in _lib.SIGNATURES) == names
+
+
+def test_default_params(L):
+    import paper_2609_36830_amd as pace
+    p = pace.default_params()
+    assert (p.w_wait, p.gamma, p.window_min, p.beta, p.r_max) == (1.0, 4, 32, 0.0, 0.9)
+
+
+def test_strerror(L):
+    assert L.pace_strerror(0) == b"ok"
+    assert b"argument" in L.pace_strerror(-1)
+    assert b"workspace" in L.pace_strerror(-2)
+
+
+def test_workspace_sizes(L):
+    import paper_2609_36830_amd as pace
+    for which in (0, 1, 2):
+        for n, nt in ((0, 0), (1, 1), (4096, 50_000_000), (20000, 1000)):
+            b = pace.pace_workspace_bytes(which, n, nt)
+            assert b >= 256 and b % 256 == 0
+    with pytest.raises(pace.PaceError):
+        pace.pace_workspace_bytes(3, 1, 1)
+    with pytest.raises(pace.PaceError):
+        pace.pace_workspace_bytes(0, -1, 1)
+
+
+def test_budget_bit_exact_vs_oracle(L):
+    """pace_budget runs on the host: compare it with the oracle everywhere."""
+    import paper_2609_36830_amd as pace
+    rng = np.random.default_rng(11)
+    cases = [(64, 48, 0.0), (4096, 1365, 0.0), (1024, 683, 0.0), (2048, 1575, 0.0), (100, 0, 0.0),
+             (0, 0, 0.0), (1, 0, 0.5), (5, 5, 0.9)]
+    for _ in range(3000):
+        N = int(rng.integers(0, 100000))
+        cases.append((N, int(rng.integers(0, N + 5)), float(rng.choice([0.0, 0.5, 0.9, 0.99, rng.random()]))))
+    for N, Nt, beta in cases:
+        rh_o = rh_g = float(rng.random()) if beta > 0 else 0.0
+        for step in range(3):
+            bo, rh_o = oracle.budget(N, Nt, rh_o, beta, 0.9)
+            bg, rh_g = pace.pace_budget(N, Nt, pace.default_params(beta=beta), rh_g)
+            assert bo == bg and rh_o == rh_g, (N, Nt, beta, step)
+
+
+def test_budget_argument_errors(L):
+    import paper_2609_36830_amd as pace
+    for kw, N, Nt, rh in (({"beta": 1.0}, 10, 5, 0.0), ({"beta": -0.1}, 10, 5, 0.0),
+                          ({"r_max": 1.5}, 10, 5, 0.0), ({}, -1, 5, 0.0), ({}, 10, -1, 0.0),
+                          ({}, 10, 5, float("nan")), ({}, 10, 5, -1.0)):
+        with pytest.raises(pace.PaceError) as e:
+            pace.pace_budget(N, Nt, pace.default_params(**kw), rh)
+        assert e.value.code == -1
+
+
+FAKE = 0x100000   # aligned, never dereferenced: each call below fails its host checks first
+
+
+def test_score_host_argument_errors(L):
+    import paper_2609_36830_amd as pace
+    p = pace.default_params()
+    P = ctypes.byref(p)
+
+    def call(tags=FAKE, off=FAKE, n=4, nt=100, comp=FAKE, V=10, pre=None, win=None, W=0, params=P,
+             out=FAKE, ws=FAKE, wsb=0):
+        return L.pace_score(tags, off, n, nt, comp, V, pre, win, W, params, out, None, None, ws, wsb, None)
+
+    assert call(off=None) == -1
+    assert call(n=-1) == -1
+    assert call(out=None) == -1
+    assert call(tags=FAKE + 2) == -1          # not 4-byte aligned
+    assert call(V=-1) == -1
+    assert call(V=2 ** 31 - 1) == -1
+    assert call(win=None, W=5) == -1
+    p.gamma = 5
+    assert call() == -1
+    p.gamma = 4
+    assert call(win=FAKE, W=10000) == -1      # 10000^4 >= 2^53
+    p.w_wait = float("nan")
+    assert call() == -1
+    p.w_wait = 1.0
+    assert call(ws=None) == -2
+    assert call(ws=FAKE + 64, wsb=1 << 30) == -2   # misaligned workspace
+    assert call(wsb=16) == -2                   # too small
+
+
+def test_select_and_compact_host_argument_errors(L):
+    assert L.pace_select(FAKE, 10, 11, FAKE, FAKE, FAKE, 1 << 20, None) == -1     # budget > n
+    assert L.pace_select(FAKE, 10, -1, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.pace_select(FAKE, 10, 3, FAKE, None, FAKE, 1 << 20, None) == -1      # no reject ids
+    assert L.pace_select(FAKE, 10, 3, FAKE, FAKE, FAKE, 0, None) == -2
+    cols = (ctypes.c_void_p * 1)(FAKE)
+    bad_e = (ctypes.c_int32 * 1)(3)
+    ok_e = (ctypes.c_int32 * 1)(4)
+    assert L.pace_compact(FAKE, 10, 100, FAKE, 1, cols, bad_e, cols, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.pace_compact(FAKE, 10, 100, FAKE, 9, cols, ok_e, cols, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.pace_compact(None, 10, 100, FAKE, 1, cols, ok_e, cols, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
+    assert L.pace_compact(FAKE, 10, 100, FAKE, 1, cols, ok_e, cols, FAKE, FAKE, FAKE, FAKE, 8, None) == -2
+    assert L.pace_validate(FAKE, None, 10, 100, FAKE, 5, None, 0, FAKE, None) == -1
