@@ -1,0 +1,211 @@
+"""Benchmark of the PACE pool filter step (score -> budget -> select -> compact)
+on one MI355X.
+
+One step is one pass of the whole filter over one pool. The workload is the
+stress pool: 4096 trajectories, log-normal lengths around 12k tokens up to
+32768 (50.1M int32 version tags), 0-16 version breaks each, V = 5000,
+occupancy 3x the target (budget 2731), scored with Effective Staleness
+(prefix window of 512, gamma 4), one int32 payload column (the tags)
+compacted into the batch. Inputs are resident in HBM before timing; before
+every timed step the L2 and MALL are flushed by reading a 512 MiB buffer
+(outside the timed events), so each step starts from cold caches.
+
+Prints ONE JSON line. Usage: python bench.py [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK = 8.0e12          # MI355X HBM3E, bytes/s
+METRIC = "pool filter step: tokens/s and trajectories/s, % of HBM peak GB/s"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", default="stress")
+    ap.add_argument("--mode", default="effective", choices=["effective", "raw", "gen"])
+    ap.add_argument("--cols", type=int, default=1, choices=[1, 3],
+                    help="payload columns: 1 = tags; 3 = tags + token ids + fp32 log-probs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run one plain 256 MiB device copy (counter calibration)")
+    return ap.parse_args()
+
+
+def alg_bytes(pool, n_keep_tok, col_bytes, W):
+    """Algorithmic bytes of one step: every tag read once, every kept token of
+    each payload column read and written once, plus the per-trajectory arrays
+    each call reads or writes (offsets, completion, prefix, score, S, T, keep,
+    reject ids, packed offsets, kept ids) and the prefix window."""
+    n, N = pool.n, pool.n_tokens
+    b = 4 * N + sum(2 * e * n_keep_tok for e in col_bytes)
+    score_call = n * (8 + 8 + 4 + 8 + 8 + 8 + 8) + 8 * W       # offsets x2, completion, prefix, score, S, T
+    select_call = n * (8 + 1) + 4 * (pool.occupancy - pool.capacity)
+    compact_call = n * (8 + 8 + 1 + 8 + 4)                      # offsets x2, keep, offsets_out, kept ids
+    return b + score_call + select_call + compact_call, 4 * N + score_call
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import poolgen
+    import paper_2609_36830_amd as pace
+    from paper_2609_36830_amd import _lib
+    if not os.path.exists(_lib.library_path):
+        from paper_2609_36830_amd import build
+        build.build()
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    pool = poolgen.make_pool(args.config)
+    D = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    tags, off, comp = D(pool.tags), D(pool.offsets), D(pool.completion)
+    prefix = None if args.mode == "raw" else D(pool.prefix_score)
+    window = None if args.mode == "raw" else D(pool.window)
+    W = 0 if window is None else window.numel()
+    host_cols = [pool.tags]
+    if args.cols == 3:
+        rng = np.random.default_rng(1)
+        host_cols += [rng.integers(0, 150000, pool.n_tokens).astype(np.int32),
+                      rng.standard_normal(pool.n_tokens).astype(np.float32)]
+    cols = [tags] + [D(c) for c in host_cols[1:]]
+    params = pace.default_params(w_wait=0.0 if args.mode == "gen" else 1.0)
+    step = pace.FilterStep(pool.n, pool.n_tokens, [c.dtype for c in cols], dev, params)
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev).view(torch.int32)
+    flush.fill_(1)
+    stream = torch.cuda.current_stream(dev)
+
+    def one_step(evs=None):
+        if evs:
+            evs[0].record(stream)
+        step.score_only(tags, off, comp, pool.V, prefix, window)
+        if evs:
+            evs[1].record(stream)
+        step.budget, _ = pace.pace_budget(pool.occupancy, pool.capacity, step.params, 0.0)
+        pace.pace_select(step.score[: pool.n], step.budget, step.keep[: pool.n], step.reject_ids, step.ws[1])
+        if evs:
+            evs[2].record(stream)
+        pace.pace_compact(off, step.keep[: pool.n], cols, [c[: pool.n_tokens] for c in step.cols_out],
+                          step.offsets_out, step.kept_ids, step.n_kept_tokens, step.ws[2],
+                          n_tokens=pool.n_tokens)
+        if evs:
+            evs[3].record(stream)
+
+    for _ in range(args.warmup):
+        flush.max()
+        one_step()
+    torch.cuda.synchronize()
+
+    # Timed region: K cold-cache steps, each bracketed by HIP events.
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        flush.max()
+        one_step(ev[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step = np.array([e[0].elapsed_time(e[3]) for e in ev])           # ms
+    per_score = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    per_select = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    per_compact = np.array([e[2].elapsed_time(e[3]) for e in ev])
+    n_keep_tok = int(step.n_kept_tokens.item())
+
+    # Warm back-to-back steps (no flush) for context.
+    warm_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    warm_ev[0].record(stream)
+    for k in range(K):
+        one_step()
+    warm_ev[1].record(stream)
+    torch.cuda.synchronize()
+    warm_ms = warm_ev[0].elapsed_time(warm_ev[1]) / K
+
+    if args.calib_copy:
+        a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(3)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    ms = float(per_step.mean())
+    B, B_score = alg_bytes(pool, n_keep_tok, [c.element_size() for c in cols], W)
+    score_ms = float(per_score.mean())
+    out = {
+        "metric": METRIC,
+        "value": pool.n_tokens / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64+f64",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s pool: %d trajectories, %d tokens, V=%d, occupancy %d, target %d, "
+                        "%s staleness, %d payload column(s), cold L2/MALL per step"
+                        % (args.config, pool.n, pool.n_tokens, pool.V, pool.occupancy,
+                           pool.capacity, args.mode, len(cols)),
+            "n_traj": pool.n, "n_tokens": pool.n_tokens, "budget": step.budget,
+            "kept_tokens": n_keep_tok, "mode": args.mode, "payload_cols": len(cols),
+            "parallelism": "single GPU",
+        },
+        "trajectories_per_s": pool.n / (ms * 1e-3),
+        "hbm_frac_of_peak": B / (ms * 1e-3) / HBM_PEAK,
+        "alg_bytes_per_step": B,
+        "ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
+        "per_call_ms": {"pace_score": score_ms, "pace_budget+pace_select": float(per_select.mean()),
+                        "pace_compact": float(per_compact.mean())},
+        "warm_ms_per_step": warm_ms,
+        "wall_s_timed_region": wall,
+        "roofline": {
+            "kernel": "pace_score (score_reduce + score_finalize)",
+            "bound": "hbm",
+            "achieved": B_score / (score_ms * 1e-3) / 1e9,
+            "peak": HBM_PEAK / 1e9,
+            "unit": "GB/s",
+            "frac": B_score / (score_ms * 1e-3) / HBM_PEAK,
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        reps, t_cpu = 0, 0.0
+        ts = time.perf_counter()
+        while reps < 3 or time.perf_counter() - ts < args.cpu_seconds:
+            oracle.filter_step(pool, mode=args.mode, cols=host_cols)
+            reps += 1
+        t_cpu = time.perf_counter() - ts
+        out["cpu_baseline"] = {
+            "value": reps * pool.n_tokens / t_cpu, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": "%d full oracle filter steps (score, budget, select, compact) on the same "
+                      "%s pool, single-threaded C, %.1f s" % (reps, args.config, t_cpu),
+        }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()
