@@ -93,7 +93,8 @@ def main():
     flush.fill_(1)
     stream = torch.cuda.current_stream(dev)
 
-    def one_step(evs=None):
+    def calls_step(evs=None):
+        """The four separate calls (per-call events)."""
         if evs:
             evs[0].record(stream)
         step.score_only(tags, off, comp, pool.V, prefix, window)
@@ -109,33 +110,54 @@ def main():
         if evs:
             evs[3].record(stream)
 
+    def fused_step(evs=None):
+        """One pace_filter_step call: the whole step in three launches."""
+        if evs:
+            evs[0].record(stream)
+        step.r_hat = 0.0
+        step.run(tags, off, comp, pool.V, pool.occupancy, pool.capacity, cols, prefix, window, fused=True)
+        if evs:
+            evs[1].record(stream)
+
     for _ in range(args.warmup):
         flush.max()
-        one_step()
+        fused_step()
+        flush.max()
+        calls_step()
     torch.cuda.synchronize()
 
-    # Timed region: K cold-cache steps, each bracketed by HIP events.
+    # Timed region: K cold-cache steps (pace_filter_step), each bracketed by HIP events.
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(K):
         flush.max()
-        one_step(ev[k])
+        fused_step(ev[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    per_step = np.array([e[0].elapsed_time(e[3]) for e in ev])           # ms
-    per_score = np.array([e[0].elapsed_time(e[1]) for e in ev])
-    per_select = np.array([e[1].elapsed_time(e[2]) for e in ev])
-    per_compact = np.array([e[2].elapsed_time(e[3]) for e in ev])
+    per_step = np.array([e[0].elapsed_time(e[1]) for e in ev])           # ms
     n_keep_tok = int(step.n_kept_tokens.item())
+    budget = step.budget
+
+    # The same step as four separate calls, for per-call times.
+    cev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+    for k in range(K):
+        flush.max()
+        calls_step(cev[k])
+    torch.cuda.synchronize()
+    calls_step_ms = np.array([e[0].elapsed_time(e[3]) for e in cev])
+    per_score = np.array([e[0].elapsed_time(e[1]) for e in cev])
+    per_select = np.array([e[1].elapsed_time(e[2]) for e in cev])
+    per_compact = np.array([e[2].elapsed_time(e[3]) for e in cev])
+    assert int(step.n_kept_tokens.item()) == n_keep_tok
 
     # Warm back-to-back steps (no flush) for context.
     warm_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
     warm_ev[0].record(stream)
     for k in range(K):
-        one_step()
+        fused_step()
     warm_ev[1].record(stream)
     torch.cuda.synchronize()
     warm_ms = warm_ev[0].elapsed_time(warm_ev[1]) / K
@@ -169,7 +191,7 @@ def main():
                         "%s staleness, %d payload column(s), cold L2/MALL per step"
                         % (args.config, pool.n, pool.n_tokens, pool.V, pool.occupancy,
                            pool.capacity, args.mode, len(cols)),
-            "n_traj": pool.n, "n_tokens": pool.n_tokens, "budget": step.budget,
+            "n_traj": pool.n, "n_tokens": pool.n_tokens, "budget": budget,
             "kept_tokens": n_keep_tok, "mode": args.mode, "payload_cols": len(cols),
             "parallelism": "single GPU",
         },
@@ -177,6 +199,8 @@ def main():
         "hbm_frac_of_peak": B / (ms * 1e-3) / HBM_PEAK,
         "alg_bytes_per_step": B,
         "ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
+        "entry": "pace_filter_step (score -> budget -> select -> compact, 3 launches)",
+        "separate_calls_ms_per_step": float(calls_step_ms.mean()),
         "per_call_ms": {"pace_score": score_ms, "pace_budget+pace_select": float(per_select.mean()),
                         "pace_compact": float(per_compact.mean())},
         "warm_ms_per_step": warm_ms,

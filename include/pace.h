@@ -9,6 +9,7 @@
  *   pace_select   reject exactly `budget` highest scores       Sec. 3.1, Algorithm 1
  *   pace_compact  pack the survivors' token spans              Algorithm 1 (batch B_j)
  *   pace_validate check the data preconditions of Lemma 1     Sec. 2, Lemma 1
+ *   pace_filter_step  all four steps above in one call        Algorithm 1
  *
  * Conventions shared by every call
  * --------------------------------
@@ -86,6 +87,7 @@ void pace_default_params(pace_params *p);
 #define PACE_WS_SCORE 0
 #define PACE_WS_SELECT 1
 #define PACE_WS_COMPACT 2
+#define PACE_WS_FILTER_STEP 3
 /* Writes to *bytes_out [host] the workspace that call needs for a pool of
  * n_traj trajectories and n_tokens tokens. Returns PACE_ERR_INVALID_ARG for
  * negative sizes or an unknown `which`. */
@@ -177,6 +179,32 @@ int pace_validate(const int32_t *tags, const int64_t *offsets, int64_t n_traj, i
                   const int32_t *completion, int32_t current_version,
                   const double *window_sorted, int64_t window_n, int32_t *err_word_out,
                   void *stream);
+
+/* pace_filter_step -- one whole trainer-side filter step (Algorithm 1):
+ * pace_budget on the host, then pace_score, pace_select and pace_compact on
+ * the device, with the same arguments and results as those four calls made
+ * in sequence (every output is bit-identical to theirs). The device work is
+ * three dependent launches instead of five: the score finalisation, the
+ * selection and the ordered scan of kept spans share one workgroup. Pools
+ * above 16384 trajectories run the separate kernels.
+ *
+ * occupancy, capacity, r_hat_inout, budget_out: as pace_budget ([host]).
+ * score_out, gen_sum_out, gen_count_out: as pace_score (gen_* may be NULL).
+ * keep_out, reject_ids_out: as pace_select (reject_ids_out holds at least
+ *   *budget_out entries; n_traj entries always suffice).
+ * n_cols .. n_kept_tokens_out: as pace_compact.
+ * workspace: pace_workspace_bytes(PACE_WS_FILTER_STEP, ...) bytes.
+ * On an argument error nothing is enqueued and *r_hat_inout is unchanged. */
+int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                     const int32_t *completion, int32_t current_version,
+                     const double *prefix_score, const double *window_sorted, int64_t window_n,
+                     int64_t occupancy, int64_t capacity, const pace_params *params,
+                     double *r_hat_inout, int64_t *budget_out, double *score_out,
+                     int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *keep_out,
+                     int32_t *reject_ids_out, int n_cols, const void *const *cols_in,
+                     const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
+                     int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
+                     size_t workspace_bytes, void *stream);
 
 /* Static description of an error code. */
 const char *pace_strerror(int code);

@@ -24,12 +24,12 @@ from ._lib import PaceParams, lib, library_path
 
 __all__ = [
     "PaceError", "PaceParams", "default_params", "pace_workspace_bytes", "pace_score",
-    "pace_budget", "pace_select", "pace_compact", "pace_validate", "FilterStep",
-    "library_path", "WS_SCORE", "WS_SELECT", "WS_COMPACT",
+    "pace_budget", "pace_select", "pace_compact", "pace_validate", "pace_filter_step", "FilterStep",
+    "library_path", "WS_SCORE", "WS_SELECT", "WS_COMPACT", "WS_FILTER_STEP",
     "BAD_OFFSETS", "BAD_COMPLETION", "BAD_TAG", "BAD_WINDOW",
 ]
 
-WS_SCORE, WS_SELECT, WS_COMPACT = 0, 1, 2
+WS_SCORE, WS_SELECT, WS_COMPACT, WS_FILTER_STEP = 0, 1, 2, 3
 BAD_OFFSETS, BAD_COMPLETION, BAD_TAG, BAD_WINDOW = 0x1, 0x2, 0x4, 0x8
 
 
@@ -200,6 +200,62 @@ def pace_validate(tags, offsets, completion, current_version, window_sorted=None
     return err_out
 
 
+def pace_filter_step(tags, offsets, completion, current_version, occupancy, capacity, cols,
+                     prefix_score=None, window_sorted=None, params: Optional[PaceParams] = None,
+                     r_hat_prev: float = 0.0, score_out=None, gen_sum_out=None, gen_count_out=None,
+                     keep_out=None, reject_ids_out=None, cols_out=None, offsets_out=None,
+                     kept_ids_out=None, n_kept_tokens_out=None, workspace=None, stream=None,
+                     with_counts=True):
+    """One whole filter step (Algorithm 1). Returns a dict with budget, r_hat and
+    the outputs of pace_score / pace_select / pace_compact (full-capacity tensors;
+    reject_ids is cut to the budget)."""
+    _dev(tags, torch.int32, "tags")
+    _dev(offsets, torch.int64, "offsets")
+    _dev(completion, torch.int32, "completion")
+    n = offsets.numel() - 1
+    nt = tags.numel()
+    dev = tags.device
+    W = 0
+    if prefix_score is not None:
+        _dev(prefix_score, torch.float64, "prefix_score")
+    if window_sorted is not None:
+        _dev(window_sorted, torch.float64, "window_sorted")
+        W = window_sorted.numel()
+    cols = list(cols)
+    for k, c in enumerate(cols):
+        if not c.is_cuda or not c.is_contiguous() or c.numel() != nt:
+            raise ValueError("column %d must be a contiguous device tensor of n_tokens elements" % k)
+    e = lambda k, dt: torch.empty(k, dtype=dt, device=dev)
+    score_out = e(n, torch.float64) if score_out is None else score_out
+    if with_counts:
+        gen_sum_out = e(n, torch.int64) if gen_sum_out is None else gen_sum_out
+        gen_count_out = e(n, torch.int64) if gen_count_out is None else gen_count_out
+    keep_out = e(n, torch.uint8) if keep_out is None else keep_out
+    reject_ids_out = e(max(n, 1), torch.int32) if reject_ids_out is None else reject_ids_out
+    cols_out = [torch.empty_like(c) for c in cols] if cols_out is None else cols_out
+    offsets_out = e(n + 1, torch.int64) if offsets_out is None else offsets_out
+    kept_ids_out = e(max(n, 1), torch.int32) if kept_ids_out is None else kept_ids_out
+    n_kept_tokens_out = e(1, torch.int64) if n_kept_tokens_out is None else n_kept_tokens_out
+    ws = _workspace(WS_FILTER_STEP, n, nt, dev, workspace)
+    nc = len(cols)
+    cin = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols])
+    cout = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols_out])
+    eb = (ctypes.c_int32 * max(nc, 1))(*[c.element_size() for c in cols])
+    rh = ctypes.c_double(float(r_hat_prev))
+    b = ctypes.c_int64(0)
+    _check(lib().pace_filter_step(_ptr(tags), _ptr(offsets), n, nt, _ptr(completion), int(current_version),
+                                  _ptr(prefix_score), _ptr(window_sorted), W, int(occupancy), int(capacity),
+                                  ctypes.byref(params) if params is not None else None,
+                                  ctypes.byref(rh), ctypes.byref(b), _ptr(score_out), _ptr(gen_sum_out),
+                                  _ptr(gen_count_out), _ptr(keep_out), _ptr(reject_ids_out), nc, cin, eb,
+                                  cout, _ptr(offsets_out), _ptr(kept_ids_out), _ptr(n_kept_tokens_out),
+                                  _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_filter_step")
+    return dict(budget=int(b.value), r_hat=float(rh.value), score=score_out, gen_sum=gen_sum_out,
+                gen_count=gen_count_out, keep=keep_out, reject_ids=reject_ids_out[: int(b.value)],
+                offsets_out=offsets_out, kept_ids=kept_ids_out, n_kept_tokens=n_kept_tokens_out,
+                cols_out=cols_out)
+
+
 class FilterStep:
     """Preallocated buffers for repeated filter steps over pools of one shape
     (n trajectories, n_tokens tokens, the given payload columns). ``run``
@@ -222,7 +278,7 @@ class FilterStep:
         self.n_kept_tokens = e(1, torch.int64)
         self.cols_out = [e(max(n_tokens, 1), dt) for dt in col_dtypes]
         self.ws = [e(max(pace_workspace_bytes(w, n, n_tokens), 256), torch.uint8)
-                   for w in (WS_SCORE, WS_SELECT, WS_COMPACT)]
+                   for w in (WS_SCORE, WS_SELECT, WS_COMPACT, WS_FILTER_STEP)]
         self.r_hat = 0.0
         self.budget = 0
 
@@ -232,7 +288,16 @@ class FilterStep:
                           self.ws[0], stream)
 
     def run(self, tags, offsets, completion, V, occupancy, capacity, cols, prefix=None,
-            window=None, stream=None):
+            window=None, stream=None, fused=True):
+        """fused: one pace_filter_step call; otherwise the four calls in sequence."""
+        if fused:
+            r = pace_filter_step(tags, offsets, completion, V, occupancy, capacity, cols, prefix, window,
+                                 self.params, self.r_hat, self.score[: self.n], self.gen_sum[: self.n],
+                                 self.gen_count[: self.n], self.keep[: self.n], self.reject_ids,
+                                 [c[: self.n_tokens] for c in self.cols_out], self.offsets_out,
+                                 self.kept_ids, self.n_kept_tokens, self.ws[3], stream)
+            self.budget, self.r_hat = r["budget"], r["r_hat"]
+            return self
         self.score_only(tags, offsets, completion, V, prefix, window, stream)
         self.budget, self.r_hat = pace_budget(occupancy, capacity, self.params, self.r_hat)
         pace_select(self.score[: self.n], self.budget, self.keep[: self.n], self.reject_ids,

@@ -26,6 +26,8 @@ SIGNATURES = [
     ("pace_select", ctypes.c_int, [P, i64, i64, P, P, P, sz, P]),
     ("pace_compact", ctypes.c_int, [P, i64, i64, P, ctypes.c_int, P, P, P, P, P, P, P, sz, P]),
     ("pace_validate", ctypes.c_int, [P, P, i64, i64, P, i32, P, i64, P, P]),
+    ("pace_filter_step", ctypes.c_int, [P, P, i64, i64, P, i32, P, P, i64, i64, i64, P, P, P, P, P, P,
+                                        P, P, ctypes.c_int, P, P, P, P, P, P, P, sz, P]),
     ("pace_strerror", ctypes.c_char_p, [ctypes.c_int]),
 ]
 

@@ -27,39 +27,60 @@ __device__ __forceinline__ int64_t readlane_i64(int64_t v, int lane) {
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-        uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, m, kWave);
-        uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), m, kWave);
-        v += ((uint64_t)hi << 32) | lo;
-    }
+// DPP moves within a wave64: row_shr:k shifts inside each 16-lane row,
+// row_bcast:15 / row_bcast:31 carry a row's last lane into the following
+// row(s). Lanes without a source (or outside row_mask) receive `old`.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, kCtrl, kRowMask, 0xf, false);
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t old, uint64_t v) {
+    const uint32_t lo = dpp_u32<kCtrl, kRowMask>((uint32_t)old, (uint32_t)v);
+    const uint32_t hi = dpp_u32<kCtrl, kRowMask>((uint32_t)(old >> 32), (uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive scan in lane order for an associative op with identity `id`
+// (row shifts 1,2,4,8, then the two row broadcasts). Lane 63 ends with the
+// reduction of the whole wave. All 64 lanes must be active.
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_scan_u32(uint32_t v, uint32_t id, Op op) {
+    v = op(v, dpp_u32<0x111, 0xf>(id, v));
+    v = op(v, dpp_u32<0x112, 0xf>(id, v));
+    v = op(v, dpp_u32<0x114, 0xf>(id, v));
+    v = op(v, dpp_u32<0x118, 0xf>(id, v));
+    v = op(v, dpp_u32<0x142, 0xa>(id, v));
+    v = op(v, dpp_u32<0x143, 0xc>(id, v));
     return v;
 }
-
-__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
-    return (int64_t)wave_sum_u64((uint64_t)v);
-}
-
-// Inclusive prefix sum across the wave (lane order).
-__device__ __forceinline__ int64_t wave_incl_scan_i64(int64_t v) {
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        uint32_t lo = (uint32_t)__shfl_up((int)(uint32_t)(uint64_t)v, d, kWave);
-        uint32_t hi = (uint32_t)__shfl_up((int)(uint32_t)((uint64_t)v >> 32), d, kWave);
-        int64_t o = (int64_t)(((uint64_t)hi << 32) | lo);
-        if (lane_id() >= d) v += o;
-    }
+template <typename Op>
+__device__ __forceinline__ uint64_t wave_scan_u64(uint64_t v, uint64_t id, Op op) {
+    v = op(v, dpp_u64<0x111, 0xf>(id, v));
+    v = op(v, dpp_u64<0x112, 0xf>(id, v));
+    v = op(v, dpp_u64<0x114, 0xf>(id, v));
+    v = op(v, dpp_u64<0x118, 0xf>(id, v));
+    v = op(v, dpp_u64<0x142, 0xa>(id, v));
+    v = op(v, dpp_u64<0x143, 0xc>(id, v));
     return v;
 }
 
 __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        uint32_t o = (uint32_t)__shfl_up((int)v, d, kWave);
-        if (lane_id() >= d) v += o;
-    }
-    return v;
+    return wave_scan_u32(v, 0u, [](uint32_t a, uint32_t b) { return a + b; });
+}
+__device__ __forceinline__ int64_t wave_incl_scan_i64(int64_t v) {
+    return (int64_t)wave_scan_u64((uint64_t)v, 0ull, [](uint64_t a, uint64_t b) { return a + b; });
+}
+// Wave-wide reductions, broadcast to every lane.
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+    return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, 0ull, [](uint64_t a, uint64_t b) { return a + b; }), kWave - 1);
+}
+__device__ __forceinline__ int64_t wave_sum_i64(int64_t v) { return (int64_t)wave_sum_u64((uint64_t)v); }
+__device__ __forceinline__ uint64_t wave_or_u64(uint64_t v) {
+    return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, 0ull, [](uint64_t a, uint64_t b) { return a | b; }), kWave - 1);
+}
+__device__ __forceinline__ uint64_t wave_and_u64(uint64_t v) {
+    return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, ~0ull, [](uint64_t a, uint64_t b) { return a & b; }), kWave - 1);
 }
 
 // Last index i in [0, n] with a[i] <= p (a non-decreasing), or -1. Every lane
@@ -82,6 +103,44 @@ __device__ __forceinline__ int64_t wave_last_le(const int64_t *__restrict__ a, i
     }
     bool le = (lane < len) && (a[base + lane] <= p);
     return base + (int64_t)__popcll(ballot(le)) - 1;
+}
+
+// Exclusive prefix sums over a block of kWaves waves in thread order; the
+// block total goes to *total. wsum: kWaves words of LDS. Two barriers.
+template <int kWaves>
+__device__ __forceinline__ uint32_t block_excl_sum_u32(uint32_t v, uint32_t &total, uint32_t *wsum) {
+    const uint32_t incl = wave_incl_scan_u32(v);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) wsum[w] = incl;
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < kWaves; ++k) {
+        const uint32_t x = wsum[k];
+        tot += x;
+        before += (k < w) ? x : 0u;
+    }
+    __syncthreads();
+    total = tot;
+    return before + incl - v;
+}
+
+template <int kWaves>
+__device__ __forceinline__ int64_t block_excl_sum_i64(int64_t v, int64_t &total, int64_t *wsum) {
+    const int64_t incl = wave_incl_scan_i64(v);
+    const int w = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) wsum[w] = incl;
+    __syncthreads();
+    int64_t before = 0, tot = 0;
+#pragma unroll
+    for (int k = 0; k < kWaves; ++k) {
+        const int64_t x = wsum[k];
+        tot += x;
+        before += (k < w) ? x : 0;
+    }
+    __syncthreads();
+    total = tot;
+    return before + incl - v;
 }
 
 __device__ __forceinline__ int64_t clamp64(int64_t v, int64_t lo, int64_t hi) {

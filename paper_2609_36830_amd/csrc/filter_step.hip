@@ -1,0 +1,58 @@
+// pace_filter_step: the whole filter step (Algorithm 1, trainer side) on
+// one stream, every phase spread over the whole device:
+//
+//   1. score_reduce   (score.hip)    every tag read once, per-chunk pieces
+//   2. score_finalize (score.hip)    one thread per trajectory: the score
+//   3. rank           (select.hip)   exact rank by counting -> keep flags
+//   4. compact_span   (compact.hip)  every workgroup rebuilds the kept-span
+//                                    scan in LDS, then copies its share of
+//                                    the batch; workgroup 0 writes the packed
+//                                    offsets, kept ids and rejected ids
+//
+// The same results as pace_score, pace_budget, pace_select and pace_compact
+// called in sequence, in four launches instead of six. Pools beyond the
+// rank and span limits use those calls' kernels.
+#include "device_util.hpp"
+#include "kernels.hpp"
+
+namespace pace {
+
+size_t filter_step_ws_bytes(int64_t n, int64_t n_tokens) {
+    return align256(score_ws_bytes(n, n_tokens)) + align256(compact_ws_bytes(n, n_tokens)) +
+           align256(select_ws_bytes(n));
+}
+
+hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                              const int32_t *completion, int32_t V, const double *prefix,
+                              const double *window, int64_t W, bool use_prefix, double w_wait,
+                              int gamma, int64_t budget, double *score, int64_t *gen_sum,
+                              int64_t *gen_count, uint8_t *keep, int32_t *reject_ids,
+                              const CompactCols &cols, int n_cols, int64_t *offsets_out,
+                              int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, bool vec_ok,
+                              hipStream_t stream) {
+    char *p = (char *)ws;
+    const ScoreWorkspace sws = score_ws_carve(p, n, n_tokens);
+    p += align256(score_ws_bytes(n, n_tokens));
+    void *cws_base = p;
+    p += align256(compact_ws_bytes(n, n_tokens));
+    void *sel_ws = p;
+
+    int64_t chunk_len = 0;
+    hipError_t e = launch_score_reduce(tags, offsets, n, n_tokens, V, sws, vec_ok, stream, &chunk_len);
+    if (e != hipSuccess) return e;
+    e = launch_score_finalize(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix,
+                              w_wait, gamma, chunk_len, score, gen_sum, gen_count, sws, stream);
+    if (e != hipSuccess) return e;
+    if (n <= kRankMaxN && compact_span_ok(n, n_tokens)) {
+        e = launch_rank(score, n, budget, keep, stream);
+        if (e != hipSuccess) return e;
+        return launch_compact_span(offsets, n, n_tokens, keep, cols, n_cols, offsets_out, kept_ids,
+                                   n_kept_tokens, reject_ids, budget, stream);
+    }
+    e = launch_select(score, n, budget, keep, reject_ids, sel_ws, stream);
+    if (e != hipSuccess) return e;
+    return launch_compact(offsets, n, n_tokens, keep, cols, n_cols, offsets_out, kept_ids,
+                          n_kept_tokens, cws_base, stream);
+}
+
+}  // namespace pace

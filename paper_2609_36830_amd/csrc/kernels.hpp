@@ -8,13 +8,26 @@
 
 namespace pace {
 
+// Waves the device keeps resident for the streaming kernels (CUs x 16).
+int64_t resident_waves();
+
 // ---- score: segmented reduction over token chunks --------------------------
-// One wave reduces one chunk of kScoreChunk consecutive tokens.
-constexpr int64_t kScoreChunk = 8192;
+// One wave reduces one chunk of consecutive tokens; the chunk length is a
+// multiple of kScoreChunkAlign chosen so that the chunks fill the device once.
+constexpr int64_t kScoreChunkAlign = 2048;
 // Largest prefix window staged in LDS by the finalize kernel.
 constexpr int64_t kWindowLdsMax = 4096;
 
-inline int64_t score_chunks(int64_t n_tokens) { return (n_tokens + kScoreChunk - 1) / kScoreChunk; }
+inline int64_t score_chunk_len(int64_t n_tokens, int64_t waves) {
+    int64_t per = (n_tokens + waves - 1) / (waves > 0 ? waves : 1);
+    per = (per + kScoreChunkAlign - 1) / kScoreChunkAlign * kScoreChunkAlign;
+    return per > kScoreChunkAlign ? per : kScoreChunkAlign;
+}
+// Upper bound on the chunk count for any device (the chunk is never shorter
+// than kScoreChunkAlign).
+inline int64_t score_max_chunks(int64_t n_tokens) {
+    return (n_tokens + kScoreChunkAlign - 1) / kScoreChunkAlign;
+}
 
 struct ScoreWorkspace {
     uint64_t *part_sum;   // [n]   sum of (tag+1) over generated tokens of the piece that starts the segment
@@ -26,6 +39,14 @@ struct ScoreWorkspace {
 size_t score_ws_bytes(int64_t n, int64_t n_tokens);
 ScoreWorkspace score_ws_carve(void *ws, int64_t n, int64_t n_tokens);
 
+hipError_t launch_score_reduce(const int32_t *tags, const int64_t *offsets, int64_t n,
+                               int64_t n_tokens, int32_t V, const ScoreWorkspace &ws, bool vec_ok,
+                               hipStream_t stream, int64_t *chunk_len_out);
+hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_tokens,
+                                 const int32_t *completion, int32_t V, const double *prefix,
+                                 const double *window, int64_t W, bool use_prefix, double w_wait,
+                                 int gamma, int64_t chunk_len, double *score, int64_t *gen_sum,
+                                 int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream);
 hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                         const int32_t *completion, int32_t V, const double *prefix,
                         const double *window, int64_t W, bool use_prefix, double w_wait, int gamma,
@@ -35,6 +56,12 @@ hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, 
 // ---- select ----------------------------------------------------------------
 constexpr int kSelectThreads = 1024;
 constexpr int kSelectMaxItems = 16;   // keys held in registers per thread
+// Pools up to this size are selected by the multi-workgroup rank-by-counting
+// kernel; larger pools by the single-workgroup radix select.
+constexpr int64_t kRankMaxN = 8192;
+// keep[i] <- 0 for the `budget` first trajectories in (score desc, id asc).
+hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,
+                       hipStream_t stream);
 size_t select_ws_bytes(int64_t n);
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
                          int32_t *reject_ids, void *ws, hipStream_t stream);
@@ -51,10 +78,40 @@ struct CompactCols {
     int32_t vec[kMaxCols];   // 1 when both pointers are 16-byte aligned
 };
 
+struct CompactWs {
+    int64_t *hdr;          // [0] kept trajectories, [1] min(kept tokens, n_tokens)
+    int64_t *kept_src;     // [n] source start of each kept span
+    int32_t *chunk_first;  // [map_capacity] kept span covering each output chunk's first element
+};
+int64_t map_capacity(int64_t n_tokens);
+CompactWs compact_ws_carve(void *ws, int64_t n, int64_t n_tokens);
 size_t compact_ws_bytes(int64_t n, int64_t n_tokens);
+hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_tokens,
+                               const int64_t *offsets_out, const CompactWs &w, hipStream_t stream);
+// Single-kernel compaction (scan rebuilt in every workgroup) for pools of at
+// most kSpanMaxN trajectories and fewer than 2^31 tokens. reject_ids may be
+// NULL; when given, the ids with keep == 0 go there in ascending order
+// (at most `budget` of them).
+constexpr int64_t kSpanMaxN = 8192;
+bool compact_span_ok(int64_t n, int64_t n_tokens);
+hipError_t launch_compact_span(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
+                               const CompactCols &cols, int n_cols, int64_t *offsets_out,
+                               int32_t *kept_ids, int64_t *n_kept_tokens, int32_t *reject_ids,
+                               int64_t budget, hipStream_t stream);
 hipError_t launch_compact(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                           const CompactCols &cols, int n_cols, int64_t *offsets_out,
                           int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, hipStream_t stream);
+
+// ---- whole filter step (fused middle kernel) --------------------------------
+size_t filter_step_ws_bytes(int64_t n, int64_t n_tokens);
+hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                              const int32_t *completion, int32_t V, const double *prefix,
+                              const double *window, int64_t W, bool use_prefix, double w_wait,
+                              int gamma, int64_t budget, double *score, int64_t *gen_sum,
+                              int64_t *gen_count, uint8_t *keep, int32_t *reject_ids,
+                              const CompactCols &cols, int n_cols, int64_t *offsets_out,
+                              int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, bool vec_ok,
+                              hipStream_t stream);
 
 // ---- validate --------------------------------------------------------------
 hipError_t launch_validate(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,

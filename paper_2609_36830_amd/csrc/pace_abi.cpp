@@ -2,6 +2,7 @@
 // argument checks, workspace carving and kernel launches. All device work is
 // enqueued on the caller's stream; nothing here allocates or synchronises.
 #include <math.h>
+#include <atomic>
 #include <stdint.h>
 #include <string.h>
 
@@ -41,6 +42,24 @@ int hip_status(hipError_t e) { return e == hipSuccess ? PACE_OK : PACE_ERR_HIP; 
 
 }  // namespace
 
+namespace pace {
+
+int64_t resident_waves() {
+    // CU count per device, queried once per device (the attribute is constant).
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256 * 16;
+    int cu = cache[dev].load(std::memory_order_relaxed);
+    if (cu <= 0) {
+        if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cu <= 0)
+            cu = 256;
+        cache[dev].store(cu, std::memory_order_relaxed);
+    }
+    return (int64_t)cu * 16;
+}
+
+}  // namespace pace
+
 extern "C" {
 
 void pace_default_params(pace_params *p) {
@@ -69,16 +88,16 @@ int pace_workspace_bytes(int which, int64_t n_traj, int64_t n_tokens, size_t *by
         case PACE_WS_SCORE: *bytes_out = score_ws_bytes(n_traj, n_tokens); return PACE_OK;
         case PACE_WS_SELECT: *bytes_out = select_ws_bytes(n_traj); return PACE_OK;
         case PACE_WS_COMPACT: *bytes_out = compact_ws_bytes(n_traj, n_tokens); return PACE_OK;
+        case PACE_WS_FILTER_STEP: *bytes_out = filter_step_ws_bytes(n_traj, n_tokens); return PACE_OK;
         default: return PACE_ERR_INVALID_ARG;
     }
 }
 
-int pace_score(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
-               const int32_t *completion, int32_t current_version, const double *prefix_score,
-               const double *window_sorted, int64_t window_n, const pace_params *params,
-               double *score_out, int64_t *gen_sum_out, int64_t *gen_count_out, void *workspace,
-               size_t workspace_bytes, void *stream) {
-    const pace_params p = params_or_default(params);
+static int check_score_args(const int32_t *tags, const int64_t *offsets, int64_t n_traj,
+                            int64_t n_tokens, const int32_t *completion, int32_t current_version,
+                            const double *prefix_score, const double *window_sorted,
+                            int64_t window_n, const pace_params &p, const double *score_out,
+                            const int64_t *gen_sum_out, const int64_t *gen_count_out) {
     if (n_traj < 0 || n_traj >= INT32_MAX || n_tokens < 0 || window_n < 0) return PACE_ERR_INVALID_ARG;
     if (!offsets || (n_traj > 0 && (!completion || !score_out)) || (n_tokens > 0 && !tags))
         return PACE_ERR_INVALID_ARG;
@@ -93,6 +112,48 @@ int pace_score(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int6
     bool of = false;
     if (window_n > 0 && (ipow_checked(window_n, p.gamma, &of) >= ((int64_t)1 << 53) || of))
         return PACE_ERR_INVALID_ARG;
+    return PACE_OK;
+}
+
+static int check_compact_args(const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                              const uint8_t *keep, int n_cols, const void *const *cols_in,
+                              const int32_t *elem_bytes, void *const *cols_out,
+                              const int64_t *offsets_out, const int32_t *kept_ids_out,
+                              const int64_t *n_kept_tokens_out, CompactCols *cols) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || n_tokens < 0 || n_cols < 0 || n_cols > kMaxCols)
+        return PACE_ERR_INVALID_ARG;
+    if (!offsets || !offsets_out || !n_kept_tokens_out || (n_traj > 0 && (!keep || !kept_ids_out)))
+        return PACE_ERR_INVALID_ARG;
+    if (!aligned(offsets, 8) || !aligned(offsets_out, 8) || !aligned(n_kept_tokens_out, 8) ||
+        !aligned(kept_ids_out, 4))
+        return PACE_ERR_INVALID_ARG;
+    if (n_cols > 0 && (!cols_in || !cols_out || !elem_bytes)) return PACE_ERR_INVALID_ARG;
+    memset(cols, 0, sizeof(*cols));
+    for (int c = 0; c < n_cols; ++c) {
+        const int32_t e = elem_bytes[c];
+        if (!(e == 1 || e == 2 || e == 4 || e == 8)) return PACE_ERR_INVALID_ARG;
+        if (n_tokens > 0 && (!cols_in[c] || !cols_out[c])) return PACE_ERR_INVALID_ARG;
+        if (!aligned(cols_in[c], (uintptr_t)e) || !aligned(cols_out[c], (uintptr_t)e))
+            return PACE_ERR_INVALID_ARG;
+        if (n_tokens > INT64_MAX / 8) return PACE_ERR_INVALID_ARG;
+        cols->in[c] = cols_in[c];
+        cols->out[c] = cols_out[c];
+        cols->elem[c] = e;
+        cols->vec[c] = (aligned(cols_in[c], 16) && aligned(cols_out[c], 16)) ? 1 : 0;
+    }
+    return PACE_OK;
+}
+
+int pace_score(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+               const int32_t *completion, int32_t current_version, const double *prefix_score,
+               const double *window_sorted, int64_t window_n, const pace_params *params,
+               double *score_out, int64_t *gen_sum_out, int64_t *gen_count_out, void *workspace,
+               size_t workspace_bytes, void *stream) {
+    const pace_params p = params_or_default(params);
+    int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
+                              prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
+                              gen_count_out);
+    if (rc != PACE_OK) return rc;
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < score_ws_bytes(n_traj, n_tokens))
         return PACE_ERR_WORKSPACE;
     const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
@@ -149,32 +210,56 @@ int pace_compact(const int64_t *offsets, int64_t n_traj, int64_t n_tokens, const
                  void *const *cols_out, int64_t *offsets_out, int32_t *kept_ids_out,
                  int64_t *n_kept_tokens_out, void *workspace, size_t workspace_bytes,
                  void *stream) {
-    if (n_traj < 0 || n_traj >= INT32_MAX || n_tokens < 0 || n_cols < 0 || n_cols > kMaxCols)
-        return PACE_ERR_INVALID_ARG;
-    if (!offsets || !offsets_out || !n_kept_tokens_out || (n_traj > 0 && (!keep || !kept_ids_out)))
-        return PACE_ERR_INVALID_ARG;
-    if (!aligned(offsets, 8) || !aligned(offsets_out, 8) || !aligned(n_kept_tokens_out, 8) ||
-        !aligned(kept_ids_out, 4))
-        return PACE_ERR_INVALID_ARG;
-    if (n_cols > 0 && (!cols_in || !cols_out || !elem_bytes)) return PACE_ERR_INVALID_ARG;
     CompactCols cols;
-    memset(&cols, 0, sizeof(cols));
-    for (int c = 0; c < n_cols; ++c) {
-        const int32_t e = elem_bytes[c];
-        if (!(e == 1 || e == 2 || e == 4 || e == 8)) return PACE_ERR_INVALID_ARG;
-        if (n_tokens > 0 && (!cols_in[c] || !cols_out[c])) return PACE_ERR_INVALID_ARG;
-        if (!aligned(cols_in[c], (uintptr_t)e) || !aligned(cols_out[c], (uintptr_t)e))
-            return PACE_ERR_INVALID_ARG;
-        if (n_tokens > INT64_MAX / 8) return PACE_ERR_INVALID_ARG;
-        cols.in[c] = cols_in[c];
-        cols.out[c] = cols_out[c];
-        cols.elem[c] = e;
-        cols.vec[c] = (aligned(cols_in[c], 16) && aligned(cols_out[c], 16)) ? 1 : 0;
-    }
+    int rc = check_compact_args(offsets, n_traj, n_tokens, keep, n_cols, cols_in, elem_bytes, cols_out,
+                                offsets_out, kept_ids_out, n_kept_tokens_out, &cols);
+    if (rc != PACE_OK) return rc;
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < compact_ws_bytes(n_traj, n_tokens))
         return PACE_ERR_WORKSPACE;
     return hip_status(launch_compact(offsets, n_traj, n_tokens, keep, cols, n_cols, offsets_out,
                                      kept_ids_out, n_kept_tokens_out, workspace, (hipStream_t)stream));
+}
+
+int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                     const int32_t *completion, int32_t current_version,
+                     const double *prefix_score, const double *window_sorted, int64_t window_n,
+                     int64_t occupancy, int64_t capacity, const pace_params *params,
+                     double *r_hat_inout, int64_t *budget_out, double *score_out,
+                     int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *keep_out,
+                     int32_t *reject_ids_out, int n_cols, const void *const *cols_in,
+                     const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
+                     int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
+                     size_t workspace_bytes, void *stream) {
+    const pace_params p = params_or_default(params);
+    int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
+                              prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
+                              gen_count_out);
+    if (rc != PACE_OK) return rc;
+    CompactCols cols;
+    rc = check_compact_args(offsets, n_traj, n_tokens, keep_out, n_cols, cols_in, elem_bytes,
+                            cols_out, offsets_out, kept_ids_out, n_kept_tokens_out, &cols);
+    if (rc != PACE_OK) return rc;
+    if (n_traj > 0 && !keep_out) return PACE_ERR_INVALID_ARG;
+    if (!r_hat_inout || !budget_out || !aligned(reject_ids_out, 4)) return PACE_ERR_INVALID_ARG;
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < filter_step_ws_bytes(n_traj, n_tokens))
+        return PACE_ERR_WORKSPACE;
+    double r_hat = *r_hat_inout;
+    int64_t budget = 0;
+    rc = pace_budget(occupancy, capacity, &p, &r_hat, &budget);
+    if (rc != PACE_OK) return rc;
+    if (budget > n_traj || (budget > 0 && !reject_ids_out)) return PACE_ERR_INVALID_ARG;
+    const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
+    const bool use_prefix = prefix_score != nullptr && window_n >= wmin;
+    rc = hip_status(launch_filter_step(tags, offsets, n_traj, n_tokens, completion, current_version,
+                                       prefix_score, window_sorted, window_n, use_prefix, p.w_wait,
+                                       p.gamma, budget, score_out, gen_sum_out, gen_count_out,
+                                       keep_out, reject_ids_out, cols, n_cols, offsets_out,
+                                       kept_ids_out, n_kept_tokens_out, workspace, aligned(tags, 16),
+                                       (hipStream_t)stream));
+    if (rc != PACE_OK) return rc;
+    *r_hat_inout = r_hat;
+    *budget_out = budget;
+    return PACE_OK;
 }
 
 int pace_validate(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,

@@ -1,8 +1,10 @@
 // pace_score kernels for gfx950.
 //
 // Step 1 (score_reduce): every per-token version tag is read exactly once.
-// The token array is cut into chunks of kScoreChunk tokens, one chunk per
-// wave64; a chunk is read as 16-byte vectors, 8 per lane in flight. The wave
+// The token array is cut into equal chunks of consecutive tokens, one per
+// wave64, sized so that every resident wave gets exactly one (a multiple of
+// 2048 tokens); a chunk is read as 16-byte vectors, 8 per lane in flight,
+// the first batch issued before the trajectory search. The wave
 // walks the trajectory boundaries that fall inside its chunk and keeps, per
 // lane, the running piece sum of (tag + 1) over generated tokens (masked
 // tags, -1, add 0) and the generated-token count. When a trajectory ends the
@@ -19,6 +21,7 @@
 // Eq. (6)-(9) in binary64 with a fixed operation order (no contraction).
 #include "device_util.hpp"
 #include "kernels.hpp"
+#include "score_math.hpp"
 
 #pragma clang fp contract(off)
 
@@ -31,7 +34,7 @@ constexpr int kWin = kWave * kVec;            // 256 tokens per wave window
 constexpr int kUnroll = 8;                    // windows in flight per wave
 constexpr int kSuper = kWin * kUnroll;        // 2048
 constexpr int kWavesPerBlock = 4;
-static_assert(kScoreChunk % kSuper == 0, "chunk must be a multiple of the super-window");
+static_assert(kScoreChunkAlign % kSuper == 0, "chunk must be a multiple of the super-window");
 
 // Lane k caches clamp(off[base + k], 0, NT); reads of increasing indices only.
 struct BoundCache {
@@ -77,18 +80,42 @@ __device__ __forceinline__ void add_range(const int4 &v, int64_t p0, int64_t lo,
     }
 }
 
+template <bool kVecLoad>
+__device__ __forceinline__ void load_super(const int32_t *__restrict__ tags, int64_t pos, int64_t ce,
+                                           int lane, int4 (&v)[kUnroll]) {
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+        const int64_t q = pos + (int64_t)k * kWin + (int64_t)lane * kVec;
+        if (kVecLoad && q + kVec <= ce) {
+            v[k] = *reinterpret_cast<const int4 *>(tags + q);
+        } else {
+            v[k] = make_int4(-1, -1, -1, -1);      // past the end: masked, adds nothing
+            if (q < ce) v[k].x = tags[q];
+            if (q + 1 < ce) v[k].y = tags[q + 1];
+            if (q + 2 < ce) v[k].z = tags[q + 2];
+            if (q + 3 < ce) v[k].w = tags[q + 3];
+        }
+    }
+}
+
 // kNarrow: every tag + 1 < 2^24, so a lane's 32 tags of one super-window sum
 // below 2^29 in 32 bits before widening.
 template <bool kNarrow, bool kVecLoad>
 __global__ __launch_bounds__(256) void score_reduce_kernel(
     const int32_t *__restrict__ tags, const int64_t *__restrict__ off, int64_t n, int64_t NT,
-    int64_t n_chunks, uint64_t *__restrict__ part_sum, int64_t *__restrict__ part_cnt,
-    uint64_t *__restrict__ carry_sum, int64_t *__restrict__ carry_cnt) {
+    int64_t chunk_len, int64_t n_chunks, uint64_t *__restrict__ part_sum,
+    int64_t *__restrict__ part_cnt, uint64_t *__restrict__ carry_sum,
+    int64_t *__restrict__ carry_cnt) {
     const int lane = lane_id();
     const int64_t chunk = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x / kWave);
     if (chunk >= n_chunks) return;
-    const int64_t cs = chunk * kScoreChunk;
-    const int64_t ce = (cs + kScoreChunk < NT) ? cs + kScoreChunk : NT;
+    const int64_t cs = chunk * chunk_len;
+    const int64_t ce = (cs + chunk_len < NT) ? cs + chunk_len : NT;
+
+    // The first super-window's loads do not depend on the trajectory search:
+    // issue them first so the search latency hides under them.
+    int4 v[kUnroll];
+    load_super<kVecLoad>(tags, cs, ce, lane, v);
 
     // Trajectory that contains the chunk's first token.
     const int64_t s = wave_last_le(off, n, cs);
@@ -133,20 +160,7 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
     };
 
     for (int64_t pos = cs; pos < ce; pos += kSuper) {
-        int4 v[kUnroll];
-#pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int64_t q = pos + (int64_t)k * kWin + (int64_t)lane * kVec;
-            if (kVecLoad && q + kVec <= ce) {
-                v[k] = *reinterpret_cast<const int4 *>(tags + q);
-            } else {
-                v[k] = make_int4(-1, -1, -1, -1);
-                if (q < ce) v[k].x = tags[q];
-                if (q + 1 < ce) v[k].y = tags[q + 1];
-                if (q + 2 < ce) v[k].z = tags[q + 2];
-                if (q + 3 < ce) v[k].w = tags[q + 3];
-            }
-        }
+        if (pos != cs) load_super<kVecLoad>(tags, pos, ce, lane, v);
         const int64_t send = (pos + kSuper < ce) ? pos + kSuper : ce;
         if (valid && cur_end >= send) {
             // Fast path: the whole super-window lies in trajectory `cur`.
@@ -199,10 +213,8 @@ template <bool kWinLds>
 __global__ __launch_bounds__(256) void score_finalize_kernel(
     const int64_t *__restrict__ off, int64_t n, int64_t NT, const int32_t *__restrict__ completion,
     int32_t V, const double *__restrict__ prefix, const double *__restrict__ window, int64_t W,
-    int use_prefix, double w_wait, int gamma, const uint64_t *__restrict__ part_sum,
-    const int64_t *__restrict__ part_cnt, const uint64_t *__restrict__ carry_sum,
-    const int64_t *__restrict__ carry_cnt, double *__restrict__ score,
-    int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count) {
+    int use_prefix, double w_wait, int gamma, int64_t chunk_len, ScoreWorkspace ws,
+    double *__restrict__ score, int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count) {
     __shared__ double win_lds[kWinLds ? kWindowLdsMax : 1];
     if (kWinLds && use_prefix) {
         for (int64_t k = threadIdx.x; k < W; k += blockDim.x) win_lds[k] = window[k];
@@ -210,59 +222,26 @@ __global__ __launch_bounds__(256) void score_finalize_kernel(
     }
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
-
     const int64_t lo = clamp64(off[i], 0, NT), hi = clamp64(off[i + 1], 0, NT);
-    uint64_t sp = 0;
-    int64_t T = 0;
-    if (hi > lo) {
-        sp = part_sum[i];
-        T = part_cnt[i];
-        for (int64_t c = lo / kScoreChunk + 1; c * kScoreChunk < hi; ++c) {
-            sp += carry_sum[c];
-            T += carry_cnt[c];
-        }
-    }
-    const int64_t c = completion[i];
-    // sp = sum(tag) + T over generated tokens; S = sum(c - tag) = c T - sum(tag).
-    const int64_t sum_tag = (int64_t)(sp - (uint64_t)T);
-    const int64_t S = c * T - sum_tag;
-
-    const double k_wait = (double)((int64_t)V - c);
-    const double k_gen = (T > 0) ? (double)S / (double)T : 0.0;
-    double F = 1.0;
-    if (use_prefix) {
-        const double sv = prefix[i];
-        if (!__builtin_isnan(sv)) {
-            int64_t a_lo = 0, a_hi = W;        // count of window entries <= sv
-            while (a_lo < a_hi) {
-                const int64_t mid = (a_lo + a_hi) >> 1;
-                const double wv = kWinLds ? win_lds[mid] : window[mid];
-                if (wv <= sv) a_lo = mid + 1; else a_hi = mid;
-            }
-            int64_t A = 1, B = 1;
-            for (int g = 0; g < gamma; ++g) {
-                A *= a_lo;
-                B *= (W - a_lo);
-            }
-            F = (double)A / (double)(A + B);
-        }
-    }
-    const double wait_term = w_wait * k_wait;
-    const double gen_term = F * k_gen;
-    score[i] = wait_term + gen_term;
-    if (gen_sum) gen_sum[i] = S;
-    if (gen_count) gen_count[i] = T;
+    const TrajPieces pc = gather_pieces(i, lo, hi, ws.part_sum, ws.part_cnt, ws.carry_sum,
+                                        ws.carry_cnt, chunk_len);
+    const TrajScore r = score_from_pieces(pc, completion[i], V, use_prefix != 0,
+                                          use_prefix ? prefix[i] : 0.0, kWinLds ? win_lds : window,
+                                          W, w_wait, gamma);
+    score[i] = r.score;
+    if (gen_sum) gen_sum[i] = r.S;
+    if (gen_count) gen_count[i] = r.T;
 }
 
 }  // namespace
 
 size_t score_ws_bytes(int64_t n, int64_t n_tokens) {
-    const int64_t ch = score_chunks(n_tokens);
+    const int64_t ch = score_max_chunks(n_tokens);
     return align256((size_t)n * 8) * 2 + align256((size_t)ch * 8) * 2 + 256;
 }
 
 ScoreWorkspace score_ws_carve(void *ws, int64_t n, int64_t n_tokens) {
-    const int64_t ch = score_chunks(n_tokens);
+    const int64_t ch = score_max_chunks(n_tokens);
     char *p = (char *)ws;
     ScoreWorkspace w;
     w.part_sum = (uint64_t *)p;  p += align256((size_t)n * 8);
@@ -272,33 +251,52 @@ ScoreWorkspace score_ws_carve(void *ws, int64_t n, int64_t n_tokens) {
     return w;
 }
 
+hipError_t launch_score_reduce(const int32_t *tags, const int64_t *offsets, int64_t n,
+                               int64_t n_tokens, int32_t V, const ScoreWorkspace &ws, bool vec_ok,
+                               hipStream_t stream, int64_t *chunk_len_out) {
+    // One contiguous, equal token range per resident wave: a single balanced
+    // round with no tail of late workgroups.
+    const int64_t chunk_len = score_chunk_len(n_tokens, resident_waves());
+    *chunk_len_out = chunk_len;
+    const int64_t ch = n_tokens > 0 ? (n_tokens + chunk_len - 1) / chunk_len : 0;
+    if (n == 0 || ch == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((ch + kWavesPerBlock - 1) / kWavesPerBlock);
+    const bool narrow = (int64_t)V < (1 << 24) - 1;
+#define PACE_REDUCE(NARROW, VEC)                                                              \
+    score_reduce_kernel<NARROW, VEC><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens,   \
+        chunk_len, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt)
+    if (narrow && vec_ok) PACE_REDUCE(true, true);
+    else if (narrow) PACE_REDUCE(true, false);
+    else if (vec_ok) PACE_REDUCE(false, true);
+    else PACE_REDUCE(false, false);
+#undef PACE_REDUCE
+    return hipGetLastError();
+}
+
+hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_tokens,
+                                 const int32_t *completion, int32_t V, const double *prefix,
+                                 const double *window, int64_t W, bool use_prefix, double w_wait,
+                                 int gamma, int64_t chunk_len, double *score, int64_t *gen_sum,
+                                 int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const unsigned grid = (unsigned)((n + 255) / 256);
+    if (use_prefix && W <= kWindowLdsMax)
+        score_finalize_kernel<true><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, 1, w_wait, gamma, chunk_len, ws, score, gen_sum, gen_count);
+    else
+        score_finalize_kernel<false><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, chunk_len, ws, score, gen_sum, gen_count);
+    return hipGetLastError();
+}
+
 hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                         const int32_t *completion, int32_t V, const double *prefix,
                         const double *window, int64_t W, bool use_prefix, double w_wait, int gamma,
                         double *score, int64_t *gen_sum, int64_t *gen_count,
                         const ScoreWorkspace &ws, bool vec_ok, hipStream_t stream) {
-    if (n == 0) return hipSuccess;
-    const int64_t ch = score_chunks(n_tokens);
-    if (ch > 0) {
-        const unsigned grid = (unsigned)((ch + kWavesPerBlock - 1) / kWavesPerBlock);
-        const bool narrow = (int64_t)V < (1 << 24) - 1;
-        if (narrow && vec_ok)
-            score_reduce_kernel<true, true><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
-        else if (narrow)
-            score_reduce_kernel<true, false><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
-        else if (vec_ok)
-            score_reduce_kernel<false, true><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
-        else
-            score_reduce_kernel<false, false><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    const unsigned grid = (unsigned)((n + 255) / 256);
-    if (use_prefix && W <= kWindowLdsMax)
-        score_finalize_kernel<true><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt, score, gen_sum, gen_count);
-    else
-        score_finalize_kernel<false><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt, score, gen_sum, gen_count);
-    return hipGetLastError();
+    int64_t chunk_len = 0;
+    hipError_t e = launch_score_reduce(tags, offsets, n, n_tokens, V, ws, vec_ok, stream, &chunk_len);
+    if (e != hipSuccess) return e;
+    return launch_score_finalize(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix,
+                                 w_wait, gamma, chunk_len, score, gen_sum, gen_count, ws, stream);
 }
 
 }  // namespace pace

@@ -4,16 +4,19 @@
 //
 // One workgroup of 1024 threads (16 waves). Each score becomes a 64-bit key
 // whose unsigned order is the score order (sign-magnitude flip; -0 -> +0).
-// An MSB-first radix select with 8-bit digits finds the budget-th largest
-// key K: each pass histograms the digit of the keys still tied with the
-// prefix found so far (LDS atomics), and a 256-bin suffix scan over four
-// waves picks the digit bin that holds the cut. The search stops early when
-// the cut falls exactly on a bin boundary. Keys above K are rejected; among
-// keys equal to K the lowest ids are rejected, found with a block-wide
-// ordered count (ballot + popcount per wave). Rejected ids are written in
-// ascending order by a second ordered count.
+// Pools of up to 16384 trajectories keep their keys in registers and use the
+// adaptive radix selection of select_block.hpp. Larger pools use the strided
+// kernel below: an MSB-first radix select with 8-bit digits finds the
+// budget-th largest key K (each pass histograms the digit of the keys still
+// tied with the prefix found so far; a 256-bin suffix scan over four waves
+// picks the bin that holds the cut; the search stops early when the cut falls
+// on a bin boundary). Keys above K are rejected; among keys equal to K the
+// lowest ids are rejected, found with a block-wide ordered count (ballot +
+// popcount per wave). Rejected ids are written in ascending order by a second
+// ordered count.
 #include "device_util.hpp"
 #include "kernels.hpp"
+#include "select_block.hpp"
 
 namespace pace {
 
@@ -22,12 +25,6 @@ namespace {
 constexpr int kT = kSelectThreads;
 constexpr int kNW = kT / kWave;   // 16 waves
 
-__device__ __forceinline__ uint64_t score_key(double d) {
-    if (__builtin_isnan(d)) return ~0ull;    // precondition violation: above +inf
-    if (d == 0.0) d = 0.0;                    // -0 and +0 are the same score
-    const uint64_t b = (uint64_t)__double_as_longlong(d);
-    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
-}
 
 // Exclusive count of `f` over the block in thread order; *total = block sum.
 __device__ __forceinline__ uint32_t block_excl_count(bool f, uint32_t &total, uint32_t *wsum) {
@@ -48,10 +45,10 @@ __device__ __forceinline__ uint32_t block_excl_count(bool f, uint32_t &total, ui
     return before + in_wave;
 }
 
-// kItems > 0: each thread holds kItems keys in registers (n <= 1024*kItems).
-// kItems == 0: keys staged in the workspace (any n < 2^31).
+// Strided layout, any n < 2^31 when kItems == 0 (keys staged in the
+// workspace). Used for pools larger than the register-resident kernel holds.
 template <int kItems>
-__global__ __launch_bounds__(kT) void select_kernel(const double *__restrict__ score, int64_t n,
+__global__ __launch_bounds__(kT) void select_strided_kernel(const double *__restrict__ score, int64_t n,
                                                     int64_t budget, uint8_t *__restrict__ keep,
                                                     int32_t *__restrict__ reject_ids,
                                                     uint64_t *__restrict__ wkeys) {
@@ -159,29 +156,153 @@ __global__ __launch_bounds__(kT) void select_kernel(const double *__restrict__ s
     }
 }
 
+
+// Register-resident selection for n <= 1024*kItems: thread t holds
+// trajectories [t*kItems, (t+1)*kItems) (see select_block.hpp), then one
+// ordered count places the rejected ids in ascending order.
+template <int kItems>
+__global__ __launch_bounds__(kT) void select_reg_kernel(const double *__restrict__ score, int64_t n,
+                                                        int64_t budget, uint8_t *__restrict__ keep,
+                                                        int32_t *__restrict__ reject_ids) {
+    __shared__ SelectSmem sm;
+    const int64_t base = (int64_t)threadIdx.x * kItems;
+    uint64_t k[kItems];
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) k[q] = score_key((base + q < n) ? score[base + q] : 0.0);
+    select_smem_init(sm);
+    bool rej[kItems];
+    select_block<kItems>(k, base, n, budget, rej, sm);
+    uint32_t nrej = 0;
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) nrej += rej[q] ? 1u : 0u;
+    uint32_t tot;
+    uint32_t pos = sel_block_excl_scan(nrej, tot, sm.wsum);
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) {
+        const int64_t i = base + q;
+        if (i < n) {
+            keep[i] = rej[q] ? 0 : 1;
+            if (rej[q]) {
+                if ((int64_t)pos < budget) reject_ids[pos] = (int32_t)i;
+                ++pos;
+            }
+        }
+    }
+}
+
+
+// ---- rank by counting (pools of up to kRankMaxN trajectories) -------------
+// rank_i = #{j : key_j > key_i} + #{j < i : key_j == key_i} is the position of
+// trajectory i in the order (score desc, id asc); it is rejected iff
+// rank_i < budget. Every workgroup (1024 threads, 16 waves per CU so LDS
+// latency hides behind other waves) stages the keys in LDS, tile by tile,
+// and ranks kRankQ trajectories with kRankS threads each; a thread counts
+// over every kRankS-th key of the tile. The n^2 comparisons spread over the
+// whole device with no dependent rounds.
+constexpr int kRankT = 1024;
+constexpr int kRankQ = 16;
+constexpr int kRankS = kRankT / kRankQ;
+constexpr int kRankTile = 4096;
+
+__global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__ score, int64_t n,
+                                                     int64_t budget, uint8_t *__restrict__ keep) {
+    __shared__ uint64_t tile[kRankTile];
+    __shared__ uint32_t part[kRankS][kRankQ + 1];
+    const int t = threadIdx.x;
+    const int q = t % kRankQ, s = t / kRankQ;
+    const int32_t i = (int32_t)((int64_t)blockIdx.x * kRankQ + q);
+    const uint64_t ki = score_key(i < n ? score[i] : 0.0);
+    uint32_t cnt = 0;
+    for (int64_t b0 = 0; b0 < n; b0 += kRankTile) {
+        const int m = (int)((n - b0) < kRankTile ? (n - b0) : kRankTile);
+        __syncthreads();
+        for (int x = t; x < m; x += kRankT) tile[x] = score_key(score[b0 + x]);
+        __syncthreads();
+        const int32_t jb = (int32_t)b0;
+        int x = s;
+        for (; x + 7 * kRankS < m; x += 8 * kRankS) {
+            uint64_t kj[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) kj[u] = tile[x + u * kRankS];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                cnt += (kj[u] > ki || (kj[u] == ki && jb + x + u * kRankS < i)) ? 1u : 0u;
+        }
+        for (; x < m; x += kRankS) {
+            const uint64_t kj = tile[x];
+            cnt += (kj > ki || (kj == ki && jb + x < i)) ? 1u : 0u;
+        }
+    }
+    part[s][q] = cnt;
+    __syncthreads();
+    if (t < kRankQ) {
+        const int64_t ii = (int64_t)blockIdx.x * kRankQ + t;
+        if (ii < n) {
+            uint32_t r = 0;
+            for (int k = 0; k < kRankS; ++k) r += part[k][t];
+            keep[ii] = ((int64_t)r < budget) ? 0 : 1;
+        }
+    }
+}
+
+// Rejected ids in ascending order from the keep flags (n <= 1024*kItems).
+template <int kItems>
+__global__ __launch_bounds__(kT) void emit_rejects_kernel(const uint8_t *__restrict__ keep, int64_t n,
+                                                          int64_t budget, int32_t *__restrict__ reject_ids) {
+    __shared__ uint32_t wsum[kNW];
+    const int64_t base = (int64_t)threadIdx.x * kItems;
+    bool rej[kItems];
+    uint32_t c = 0;
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) {
+        rej[q] = base + q < n && keep[base + q] == 0;
+        c += rej[q] ? 1u : 0u;
+    }
+    uint32_t tot;
+    uint32_t pos = block_excl_sum_u32<kNW>(c, tot, wsum);
+#pragma unroll
+    for (int q = 0; q < kItems; ++q) {
+        if (rej[q]) {
+            if ((int64_t)pos < budget) reject_ids[pos] = (int32_t)(base + q);
+            ++pos;
+        }
+    }
+}
+
 }  // namespace
 
 size_t select_ws_bytes(int64_t n) {
     return (n > (int64_t)kT * kSelectMaxItems) ? align256((size_t)n * 8) : 256;
 }
 
+hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,
+                       hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    rank_kernel<<<(unsigned)((n + kRankQ - 1) / kRankQ), kRankT, 0, stream>>>(score, n, budget, keep);
+    return hipGetLastError();
+}
+
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
                          int32_t *reject_ids, void *ws, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     const int64_t items = (n + kT - 1) / kT;
-    uint64_t *wk = (uint64_t *)ws;
-    if (items <= 1)
-        select_kernel<1><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
-    else if (items <= 2)
-        select_kernel<2><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
-    else if (items <= 4)
-        select_kernel<4><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
-    else if (items <= 8)
-        select_kernel<8><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
-    else if (items <= 16)
-        select_kernel<16><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+    if (n <= kRankMaxN) {
+        hipError_t e = launch_rank(score, n, budget, keep, stream);
+        if (e != hipSuccess || budget == 0) return e;
+        if (items <= 1)
+            emit_rejects_kernel<1><<<1, kT, 0, stream>>>(keep, n, budget, reject_ids);
+        else if (items <= 2)
+            emit_rejects_kernel<2><<<1, kT, 0, stream>>>(keep, n, budget, reject_ids);
+        else if (items <= 4)
+            emit_rejects_kernel<4><<<1, kT, 0, stream>>>(keep, n, budget, reject_ids);
+        else
+            emit_rejects_kernel<8><<<1, kT, 0, stream>>>(keep, n, budget, reject_ids);
+        return hipGetLastError();
+    }
+    if (items <= 16)
+        select_reg_kernel<16><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids);
     else
-        select_kernel<0><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, wk);
+        select_strided_kernel<0><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, (uint64_t *)ws);
     return hipGetLastError();
 }
 

@@ -33,7 +33,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for f in ("pace_score", "pace_budget", "pace_select", "pace_compact", "pace_validate",
-              "pace_workspace_bytes", "pace_default_params", "pace_strerror"):
+              "pace_filter_step", "pace_workspace_bytes", "pace_default_params", "pace_strerror"):
         assert f in names
 
 
@@ -59,12 +59,12 @@ def test_strerror(L):
 
 def test_workspace_sizes(L):
     import paper_2609_36830_amd as pace
-    for which in (0, 1, 2):
+    for which in (0, 1, 2, 3):
         for n, nt in ((0, 0), (1, 1), (4096, 50_000_000), (20000, 1000)):
             b = pace.pace_workspace_bytes(which, n, nt)
             assert b >= 256 and b % 256 == 0
     with pytest.raises(pace.PaceError):
-        pace.pace_workspace_bytes(3, 1, 1)
+        pace.pace_workspace_bytes(4, 1, 1)
     with pytest.raises(pace.PaceError):
         pace.pace_workspace_bytes(0, -1, 1)
 
@@ -125,6 +125,31 @@ def test_score_host_argument_errors(L):
     assert call(ws=None) == -2
     assert call(ws=FAKE + 64, wsb=1 << 30) == -2   # misaligned workspace
     assert call(wsb=16) == -2                   # too small
+
+
+def test_filter_step_host_argument_errors(L):
+    """pace_filter_step rejects bad arguments before enqueuing, r_hat untouched."""
+    import paper_2609_36830_amd as pace
+    p = pace.default_params()
+    rh = ctypes.c_double(0.25)
+    b = ctypes.c_int64(-7)
+    cols = (ctypes.c_void_p * 1)(FAKE)
+    e4 = (ctypes.c_int32 * 1)(4)
+
+    def call(occ=10, cap=5, ws=FAKE, wsb=1 << 30, keep=FAKE, rej=FAKE, beta=0.0, n=4):
+        p.beta = beta
+        return L.pace_filter_step(FAKE, FAKE, n, 100, FAKE, 10, None, None, 0, occ, cap, ctypes.byref(p),
+                                  ctypes.byref(rh), ctypes.byref(b), FAKE, None, None, keep, rej, 1, cols, e4,
+                                  cols, FAKE, FAKE, FAKE, ws, wsb, None)
+
+    assert call(keep=None) == -1
+    assert call(beta=1.5) == -1
+    assert call(occ=-1) == -1
+    assert call(occ=100, cap=0, n=4) == -1      # budget 90 > 4 trajectories
+    assert call(rej=None) == -1
+    assert call(ws=None) == -2
+    assert call(wsb=64) == -2
+    assert rh.value == 0.25 and b.value == -7
 
 
 def test_select_and_compact_host_argument_errors(L):

@@ -49,12 +49,25 @@ def H(t):
     return t.detach().cpu().numpy()
 
 
-def gpu_step(pace, pool, mode="effective", cols=None, params=None, r_hat_prev=0.0):
+def gpu_step(pace, pool, mode="effective", cols=None, params=None, r_hat_prev=0.0, fused=False):
+    """One filter step through the C ABI: the four separate calls, or
+    pace_filter_step when fused."""
     params = params or pace.default_params(w_wait=0.0 if mode == "gen" else 1.0)
     tags, off, comp = D(pool.tags), D(pool.offsets), D(pool.completion)
     prefix = None if mode == "raw" else D(pool.prefix_score)
     window = None if mode == "raw" else D(pool.window)
     cols_d = [tags] if cols is None else [D(c) for c in cols]
+    if fused:
+        r = pace.pace_filter_step(tags, off, comp, pool.V, pool.occupancy, pool.capacity, cols_d, prefix,
+                                  window, params, r_hat_prev)
+        torch.cuda.synchronize()
+        b = r["budget"]
+        n_kept = pool.n - b
+        nk = int(H(r["n_kept_tokens"])[0])
+        return dict(score=H(r["score"]), S=H(r["gen_sum"]), T=H(r["gen_count"]), budget=b, r_hat=r["r_hat"],
+                    keep=H(r["keep"]), reject_ids=H(r["reject_ids"]), offsets_out=H(r["offsets_out"])[: n_kept + 1],
+                    kept_ids=H(r["kept_ids"])[:n_kept], n_kept_tokens=nk,
+                    packed=[H(p)[:nk] for p in r["cols_out"]])
     sc, S, T = pace.pace_score(tags, off, comp, pool.V, prefix, window, params)
     b, rh = pace.pace_budget(pool.occupancy, pool.capacity, params, r_hat_prev)
     keep, rej = pace.pace_select(sc, b)
@@ -91,32 +104,39 @@ def oracle_step(pool, mode="effective", cols=None, r_hat_prev=0.0, beta=0.0, gam
 # ---------------------------------------------------------------------------
 # The paper-shaped pools at their full sizes
 # ---------------------------------------------------------------------------
+FUSED = pytest.mark.parametrize("fused", [False, True], ids=["calls", "fused"])
+
+
+@FUSED
 @pytest.mark.parametrize("name", ["tiny", "math", "long", "multiturn"])
 @pytest.mark.parametrize("mode", ["effective", "raw", "gen"])
-def test_pool_parity(pace, name, mode):
+def test_pool_parity(pace, name, mode, fused):
     pool = poolgen.make_pool(name)
-    say("pool %s mode %s n=%d tokens=%d" % (name, mode, pool.n, pool.n_tokens))
-    assert_same(gpu_step(pace, pool, mode), oracle_step(pool, mode), "%s/%s" % (name, mode))
+    say("pool %s mode %s fused %s n=%d tokens=%d" % (name, mode, fused, pool.n, pool.n_tokens))
+    assert_same(gpu_step(pace, pool, mode, fused=fused), oracle_step(pool, mode), "%s/%s" % (name, mode))
 
 
+@FUSED
 @pytest.mark.parametrize("mode", ["effective", "raw"])
-def test_stress_pool_parity(pace, mode):
+def test_stress_pool_parity(pace, mode, fused):
     pool = poolgen.make_pool("stress")
-    say("stress %s n=%d tokens=%d" % (mode, pool.n, pool.n_tokens))
-    g = gpu_step(pace, pool, mode)
+    say("stress %s fused %s n=%d tokens=%d" % (mode, fused, pool.n, pool.n_tokens))
+    g = gpu_step(pace, pool, mode, fused=fused)
     assert_same(g, oracle_step(pool, mode), "stress/" + mode)
     assert g["budget"] == 2731
 
 
+@FUSED
 @pytest.mark.parametrize("seed", [7, 8, 9])
 @pytest.mark.parametrize("name", ["tiny", "math", "multiturn"])
-def test_other_seeds(pace, name, seed):
+def test_other_seeds(pace, name, seed, fused):
     pool = poolgen.make_pool(name, seed=seed, n=512 if name != "tiny" else None)
-    say("seed %d pool %s" % (seed, name))
-    assert_same(gpu_step(pace, pool), oracle_step(pool), "%s seed %d" % (name, seed))
+    say("seed %d pool %s fused %s" % (seed, name, fused))
+    assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), "%s seed %d" % (name, seed))
 
 
-def test_multi_column_payload(pace):
+@FUSED
+def test_multi_column_payload(pace, fused):
     """Tags plus token ids (int32), behavior log-probs (fp32), a loss mask
     (uint8), positions (int16) and fp64 values, as separate columns."""
     pool = poolgen.make_pool("multiturn", n=700)
@@ -126,7 +146,7 @@ def test_multi_column_payload(pace):
             (pool.tags != -1).astype(np.uint8), (np.arange(N) % 30000).astype(np.int16),
             rng.standard_normal(N)]
     say("multi-column n=%d tokens=%d" % (pool.n, N))
-    assert_same(gpu_step(pace, pool, cols=cols), oracle_step(pool, cols=cols), "multi-column")
+    assert_same(gpu_step(pace, pool, cols=cols, fused=fused), oracle_step(pool, cols=cols), "multi-column")
 
 
 # ---------------------------------------------------------------------------
@@ -145,22 +165,33 @@ EDGE_LENGTHS = {
 }
 
 
+@FUSED
 @pytest.mark.parametrize("case", sorted(EDGE_LENGTHS))
 @pytest.mark.parametrize("mask_frac", [0.0, 0.35])
-def test_edge_shapes(pace, case, mask_frac):
+def test_edge_shapes(pace, case, mask_frac, fused):
     lens = EDGE_LENGTHS[case]
     pool = poolgen.make_custom_pool(lens, V=40, seed=len(lens) + 17, mask_frac=mask_frac, W=64)
-    say("edge %s mask %.2f n=%d tokens=%d" % (case, mask_frac, pool.n, pool.n_tokens))
-    assert_same(gpu_step(pace, pool), oracle_step(pool), case)
+    say("edge %s mask %.2f fused %s n=%d tokens=%d" % (case, mask_frac, fused, pool.n, pool.n_tokens))
+    assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), case)
 
 
-def test_all_masked_trajectories(pace):
+@FUSED
+def test_pool_above_register_capacity(pace, fused):
+    """20000 trajectories: the fused call falls back to the separate kernels."""
+    lens = np.random.default_rng(9).integers(0, 400, size=20000)
+    pool = poolgen.make_custom_pool(lens, V=60, seed=99, mask_frac=0.1, W=512)
+    say("n=20000 fused %s" % fused)
+    assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), "n=20000")
+
+
+@FUSED
+def test_all_masked_trajectories(pace, fused):
     pool = poolgen.make_custom_pool([500, 0, 300, 1000], V=30, seed=4, W=64)
     pool.tags[:500] = -1
     pool.tags[800:1800] = -1
     r = oracle_step(pool)
     assert r["T"][0] == 0 and r["T"][3] == 0
-    assert_same(gpu_step(pace, pool), r, "all-masked")
+    assert_same(gpu_step(pace, pool, fused=fused), r, "all-masked")
 
 
 def test_unaligned_tags_take_the_scalar_path(pace):
@@ -182,51 +213,56 @@ def test_unaligned_tags_take_the_scalar_path(pace):
     assert np.array_equal(H(packed[0])[: r["n_kept_tokens"]], r["packed"][0])
 
 
-def test_large_versions_take_the_wide_path(pace):
+@FUSED
+def test_large_versions_take_the_wide_path(pace, fused):
     lens = [700, 20000, 5, 9000]
     pool = poolgen.make_custom_pool(lens, V=2 ** 30, seed=12, mask_frac=0.1, W=64)
-    say("wide versions V=2^30")
-    assert_same(gpu_step(pace, pool), oracle_step(pool), "wide")
+    say("wide versions V=2^30 fused %s" % fused)
+    assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), "wide")
 
 
+@FUSED
 @pytest.mark.parametrize("gamma", [1, 2, 3, 4])
-def test_gamma_and_window_min(pace, gamma):
+def test_gamma_and_window_min(pace, gamma, fused):
     pool = poolgen.make_pool("math", n=400)
     for wmin in (0, 32, 600):
         params = pace.default_params(gamma=gamma, window_min=wmin)
-        say("gamma %d window_min %d" % (gamma, wmin))
-        g = gpu_step(pace, pool, params=params)
+        say("gamma %d window_min %d fused %s" % (gamma, wmin, fused))
+        g = gpu_step(pace, pool, params=params, fused=fused)
         r = oracle_step(pool, gamma=gamma, window_min=wmin)
         assert_same(g, r, "gamma %d wmin %d" % (gamma, wmin))
 
 
-def test_large_window_in_global_memory(pace):
+@FUSED
+def test_large_window_in_global_memory(pace, fused):
     """A 6000-entry prefix window (beyond the LDS-staged size), gamma = 1."""
     pool = poolgen.make_custom_pool(np.full(300, 100), V=50, seed=21, W=6000)
     params = pace.default_params(gamma=1)
-    say("window 6000")
-    assert_same(gpu_step(pace, pool, params=params), oracle_step(pool, gamma=1), "big window")
+    say("window 6000 fused %s" % fused)
+    assert_same(gpu_step(pace, pool, params=params, fused=fused), oracle_step(pool, gamma=1), "big window")
 
 
-def test_budget_extremes(pace):
+@FUSED
+def test_budget_extremes(pace, fused):
     pool = poolgen.make_pool("tiny")
     for cap, rmax in ((64, 0.9), (200, 0.9), (0, 1.0), (0, 0.9), (63, 0.9)):
         pool.capacity = cap
         params = pace.default_params(r_max=rmax)
-        say("budget capacity %d r_max %.1f" % (cap, rmax))
-        g = gpu_step(pace, pool, params=params)
+        say("budget capacity %d r_max %.1f fused %s" % (cap, rmax, fused))
+        g = gpu_step(pace, pool, params=params, fused=fused)
         r = oracle_step(pool, r_max=rmax)
         assert_same(g, r, "capacity %d" % cap)
 
 
-def test_ema_sequence(pace):
+@FUSED
+def test_ema_sequence(pace, fused):
     """beta = 0.9 across consecutive steps: r_hat threads through the host call."""
     pool = poolgen.make_pool("tiny")
     rg = ro = 0.0
     for occ in (64, 64, 60, 55, 49, 48, 40, 64):
         pool.occupancy = occ
         params = pace.default_params(beta=0.9)
-        g = gpu_step(pace, pool, params=params, r_hat_prev=rg)
+        g = gpu_step(pace, pool, params=params, r_hat_prev=rg, fused=fused)
         r = oracle_step(pool, beta=0.9, r_hat_prev=ro)
         assert_same(g, r, "ema occ %d" % occ)
         rg, ro = g["r_hat"], r["r_hat"]
@@ -305,12 +341,13 @@ def test_validate_flags(pace):
 # ---------------------------------------------------------------------------
 # Determinism: identical bits run to run
 # ---------------------------------------------------------------------------
-def test_repeat_runs_identical(pace):
+@FUSED
+def test_repeat_runs_identical(pace, fused):
     pool = poolgen.make_pool("long")
-    say("determinism x5 on long pool")
-    first = gpu_step(pace, pool)
+    say("determinism x5 on long pool fused %s" % fused)
+    first = gpu_step(pace, pool, fused=fused)
     for _ in range(4):
-        again = gpu_step(pace, pool)
+        again = gpu_step(pace, pool, fused=fused)
         for k in ("score", "S", "T", "keep", "reject_ids", "offsets_out", "kept_ids"):
             assert np.array_equal(first[k], again[k]), k
         assert np.array_equal(first["packed"][0], again["packed"][0])
