@@ -199,7 +199,7 @@ def main():
         "hbm_frac_of_peak": B / (ms * 1e-3) / HBM_PEAK,
         "alg_bytes_per_step": B,
         "ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
-        "entry": "pace_filter_step (score -> budget -> select -> compact, 3 launches)",
+        "entry": "pace_filter_step (score -> budget -> select -> compact, 4 launches)",
         "separate_calls_ms_per_step": float(calls_step_ms.mean()),
         "per_call_ms": {"pace_score": score_ms, "pace_budget+pace_select": float(per_select.mean()),
                         "pace_compact": float(per_compact.mean())},

@@ -2,9 +2,11 @@
 // into the training batch (Algorithm 1), survivors in pool order.
 //
 // Copy routine (both paths): a wave copies a contiguous range of output
-// elements. Output goes out as aligned 16-byte vectors (64 lanes x 16 B =
-// 1 KiB per wave window, four windows in flight). Inside one kept span the
-// source is the destination shifted by a constant, so the source
+// elements. Output goes out as aligned 16-byte non-temporal vectors (64 lanes
+// x 16 B = 1 KiB per wave window, four windows in flight); sources are read
+// with plain loads, since the kept spans are often still in the last-level
+// cache from the scoring pass. Inside one kept span the source is the
+// destination shifted by a constant, so the source
 // misalignment is wave-uniform: each lane loads the aligned 16 bytes under
 // its window, takes the next 16 bytes from the neighbouring lane (lane 63
 // loads them), and a byte funnel shift assembles the output vector. Windows
@@ -139,7 +141,7 @@ __device__ void copy_range(const char *__restrict__ in, char *__restrict__ out, 
                     if (lane == kWave - 1) b = x[u];
                     o = funnel16(a[u], b, shift);
                 }
-                *reinterpret_cast<uint4 *>(out + (w + (int64_t)u * WE + (int64_t)lane * VE) * E) = o;
+                store_nt(reinterpret_cast<uint4 *>(out + (w + (int64_t)u * WE + (int64_t)lane * VE) * E), o);
             }
             w += (U - 1) * WE;
             continue;
@@ -153,7 +155,7 @@ __device__ void copy_range(const char *__restrict__ in, char *__restrict__ out, 
                 if (lane == kWave - 1) b = *reinterpret_cast<const uint4 *>(in + ab + 16);
                 o = funnel16(a, b, shift);
             }
-            *reinterpret_cast<uint4 *>(out + (w + (int64_t)lane * VE) * E) = o;
+            store_nt(reinterpret_cast<uint4 *>(out + (w + (int64_t)lane * VE) * E), o);
             continue;
         }
         // Element path: every span that meets [w, we).

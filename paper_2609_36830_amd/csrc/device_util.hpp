@@ -143,6 +143,23 @@ __device__ __forceinline__ int64_t block_excl_sum_i64(int64_t v, int64_t &total,
     return before + incl - v;
 }
 
+// Streaming (non-temporal) 16-byte accesses: data touched once per step
+// should not displace reusable lines from L2 and MALL.
+typedef int pace_v4i __attribute__((ext_vector_type(4)));
+typedef unsigned pace_v4u __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ int4 load_nt(const int4 *p) {
+    const pace_v4i x = __builtin_nontemporal_load(reinterpret_cast<const pace_v4i *>(p));
+    return make_int4(x.x, x.y, x.z, x.w);
+}
+__device__ __forceinline__ uint4 load_nt(const uint4 *p) {
+    const pace_v4u x = __builtin_nontemporal_load(reinterpret_cast<const pace_v4u *>(p));
+    return make_uint4(x.x, x.y, x.z, x.w);
+}
+__device__ __forceinline__ void store_nt(uint4 *p, const uint4 &v) {
+    const pace_v4u x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<pace_v4u *>(p));
+}
+
 __device__ __forceinline__ int64_t clamp64(int64_t v, int64_t lo, int64_t hi) {
     return v < lo ? lo : (v > hi ? hi : v);
 }

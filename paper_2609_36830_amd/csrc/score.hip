@@ -3,8 +3,10 @@
 // Step 1 (score_reduce): every per-token version tag is read exactly once.
 // The token array is cut into equal chunks of consecutive tokens, one per
 // wave64, sized so that every resident wave gets exactly one (a multiple of
-// 2048 tokens); a chunk is read as 16-byte vectors, 8 per lane in flight,
-// the first batch issued before the trajectory search. The wave
+// 2048 tokens); a chunk is read as 16-byte vectors, 8 per lane in flight, the
+// first batch issued before the trajectory search. (Plain loads on purpose:
+// they leave the tags in the last-level cache, where the compaction re-reads
+// the kept spans.) The wave
 // walks the trajectory boundaries that fall inside its chunk and keeps, per
 // lane, the running piece sum of (tag + 1) over generated tokens (masked
 // tags, -1, add 0) and the generated-token count. When a trajectory ends the
