@@ -206,6 +206,26 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
                      int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
                      size_t workspace_bytes, void *stream);
 
+/* pace_time_next_kernel -- measurement hook, not part of the method.
+ * Arms a one-shot timer for one phase of the device work on the calling host
+ * thread: the next kernel of that phase launched from this thread (by any
+ * entry point, on any stream) is launched with hipExtLaunchKernel and the two
+ * events, so that hipEventElapsedTime(start, stop) afterwards gives that
+ * kernel's own execution time. The launch consumes the timer.
+ * phase: PACE_PHASE_REDUCE (token reduction of pace_score), PACE_PHASE_FINALIZE
+ *   (score finalisation), PACE_PHASE_SELECT (the rank kernel, or the
+ *   single-workgroup select of large pools), PACE_PHASE_COMPACT (the
+ *   compaction copy kernel).
+ * start_event, stop_event: hipEvent_t handles created by the caller with
+ *   timing enabled; both NULL disarms the phase. The caller keeps ownership.
+ * Returns PACE_ERR_INVALID_ARG for an unknown phase or one NULL event. */
+#define PACE_PHASE_REDUCE 0
+#define PACE_PHASE_FINALIZE 1
+#define PACE_PHASE_SELECT 2
+#define PACE_PHASE_COMPACT 3
+#define PACE_PHASE_COUNT 4
+int pace_time_next_kernel(int phase, void *start_event, void *stop_event);
+
 /* Static description of an error code. */
 const char *pace_strerror(int code);
 

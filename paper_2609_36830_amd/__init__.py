@@ -31,6 +31,7 @@ __all__ = [
 
 WS_SCORE, WS_SELECT, WS_COMPACT, WS_FILTER_STEP = 0, 1, 2, 3
 BAD_OFFSETS, BAD_COMPLETION, BAD_TAG, BAD_WINDOW = 0x1, 0x2, 0x4, 0x8
+PHASE_REDUCE, PHASE_FINALIZE, PHASE_SELECT, PHASE_COMPACT = 0, 1, 2, 3
 
 
 class PaceError(RuntimeError):
@@ -254,6 +255,20 @@ def pace_filter_step(tags, offsets, completion, current_version, occupancy, capa
                 gen_count=gen_count_out, keep=keep_out, reject_ids=reject_ids_out[: int(b.value)],
                 offsets_out=offsets_out, kept_ids=kept_ids_out, n_kept_tokens=n_kept_tokens_out,
                 cols_out=cols_out)
+
+
+def pace_time_next_kernel(phase: int, start=None, stop=None):
+    """Arm a one-shot timer on the next kernel of `phase` launched from this
+    thread. start/stop are torch.cuda.Event(enable_timing=True) objects that
+    have been recorded once (so that their HIP events exist); None for both
+    disarms. Afterwards start.elapsed_time(stop) is that kernel's own time."""
+    def handle(ev):
+        if ev is None:
+            return None
+        if not ev.cuda_event:
+            raise PaceError(-1, "pace_time_next_kernel (record the event once before arming it)")
+        return ev.cuda_event
+    _check(_lib.lib().pace_time_next_kernel(int(phase), handle(start), handle(stop)), "pace_time_next_kernel")
 
 
 class FilterStep:

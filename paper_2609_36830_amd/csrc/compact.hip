@@ -13,13 +13,17 @@
 // that straddle span ends, the ragged tail and unaligned columns copy element
 // by element.
 //
-// Span path (n <= kSpanMaxN, n_tokens < 2^31): ONE kernel. Every 1024-thread
-// workgroup (one per CU) first rebuilds the ordered scan of keep flags and
-// kept lengths for the whole pool in LDS -- a few kilobytes from L2, one
-// block scan -- then its waves copy equal shares of the packed batch,
-// locating their first span by a search in LDS. Workgroup 0 also writes the
-// packed offsets, kept ids, the kept-token count and (when asked) the
-// rejected ids.
+// Piece path (n <= kPieceMaxN): consecutive trajectories form blocks of
+// kPieceBlock; per block the rank kernel (or compact_partials_kernel) has
+// written the kept count, kept tokens and the number of pieces of at most
+// kPieceLen tokens the kept spans cut into. The copy kernel then runs one
+// 256-thread workgroup per block, writing that block's packed offsets, kept
+// ids and rejected ids, and one per piece: the workgroup scans the block
+// partials (at most 512) to find its block, the 16 trajectories of the block
+// to find its span, and copies the piece with 16-byte vectors (source loads
+// dword-aligned, stores aligned and non-temporal). Pieces are short enough
+// that long trajectories spread over many workgroups, long enough that the
+// per-workgroup set-up is small next to the copy.
 //
 // Scan path (larger pools): one workgroup scans the flags into the packed
 // offsets, kept ids, span sources and a map from each output chunk of
@@ -54,15 +58,6 @@ struct GlobalSpans {
     }
     __device__ __forceinline__ int64_t O(int64_t j) const { return readlane_i64(o, (int)(j - base)); }
     __device__ __forceinline__ int64_t S(int64_t j) const { return readlane_i64(s, (int)(j - base)); }
-};
-
-// LDS arrays (int32: the span path requires n_tokens < 2^31).
-struct LdsSpans {
-    const int32_t *kdst;   // [n_kept + 1]
-    const int32_t *ksrc;   // [n_kept]
-    __device__ __forceinline__ void ensure(int64_t) {}
-    __device__ __forceinline__ int64_t O(int64_t j) const { return kdst[j]; }
-    __device__ __forceinline__ int64_t S(int64_t j) const { return ksrc[j]; }
 };
 
 template <int E> struct Elem;
@@ -196,95 +191,196 @@ __device__ __forceinline__ void copy_range_col(const CompactCols &cols, int col,
 }
 
 // ---------------------------------------------------------------------------
-// Span path
+// Piece path
 // ---------------------------------------------------------------------------
-// Last j in [0, m) with a[j] <= p (a non-decreasing, LDS), or 0.
-__device__ __forceinline__ int64_t lds_last_le(const int32_t *a, int64_t m, int64_t p) {
-    int64_t lo = 0, hi = m;           // answer in [lo, hi)
-    while (hi - lo > 1) {
-        const int64_t mid = (lo + hi) >> 1;
-        if ((int64_t)a[mid] <= p) lo = mid; else hi = mid;
-    }
-    return lo;
+constexpr int kPT = 256;                  // threads of a piece workgroup
+constexpr int kPW = kPT / kWave;          // its waves
+constexpr int kPartsPerThread = (int)((kPieceMaxN / kPieceBlock + kPT - 1) / kPT);
+
+// Span length of trajectory i if kept (offsets clamped to [0, NT]), else 0.
+__device__ __forceinline__ int64_t kept_span(const int64_t *__restrict__ off, const uint8_t *__restrict__ keep,
+                                             int64_t i, int64_t NT, int64_t &lo) {
+    lo = 0;
+    if (keep[i] == 0) return -1;
+    lo = clamp64(off[i], 0, NT);
+    const int64_t hi = clamp64(off[i + 1], 0, NT);
+    return hi > lo ? hi - lo : 0;
 }
 
-template <int kItems>
-__global__ __launch_bounds__(kT) void compact_span_kernel(
-    const int64_t *__restrict__ off, int64_t n, int64_t NT, const uint8_t *__restrict__ keep,
-    CompactCols cols, int n_cols, int64_t *__restrict__ offsets_out, int32_t *__restrict__ kept_ids,
-    int64_t *__restrict__ n_kept_tokens, int32_t *__restrict__ reject_ids, int64_t budget) {
-    __shared__ int32_t kdst[kItems * kT + 1];
-    __shared__ int32_t ksrc[kItems * kT];
-    __shared__ uint32_t wcnt[kNW], wrej[kNW];
-    __shared__ int64_t wlen[kNW];
-    const bool writer = blockIdx.x == 0;
-    const int64_t base = (int64_t)threadIdx.x * kItems;
+// One wave per block: the block partials from the keep flags.
+__global__ __launch_bounds__(kWave) void compact_partials_kernel(const int64_t *__restrict__ off, int64_t n,
+                                                                int64_t NT, const uint8_t *__restrict__ keep,
+                                                                PieceParts parts) {
+    const int lane = lane_id();
+    const int64_t i = (int64_t)blockIdx.x * kPieceBlock + lane;
+    int64_t len = 0, lo;
+    bool kept = false;
+    if (lane < kPieceBlock && i < n) {
+        const int64_t k = kept_span(off, keep, i, NT, lo);
+        kept = k >= 0;
+        len = kept ? k : 0;
+    }
+    const uint32_t c = (uint32_t)__popcll(ballot(kept));
+    const int64_t l = wave_sum_i64(len);
+    const int64_t pc = wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
+    if (lane == 0) {
+        parts.cnt[blockIdx.x] = (int32_t)c;
+        parts.len[blockIdx.x] = l;
+        parts.pcs[blockIdx.x] = (int32_t)pc;
+    }
+}
 
-    // 1. Ordered scan of the keep flags and kept lengths, in every workgroup.
-    int64_t o[kItems + 1];
-    bool kp[kItems];
-#pragma unroll
-    for (int q = 0; q <= kItems; ++q) o[q] = (base + q <= n) ? clamp64(off[base + q], 0, NT) : 0;
-#pragma unroll
-    for (int q = 0; q < kItems; ++q) kp[q] = (base + q < n) && keep[base + q] != 0;
-    uint32_t c = 0, r = 0;
-    int64_t l = 0;
-#pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-        if (kp[q]) {
-            c += 1;
-            l += (o[q + 1] > o[q]) ? o[q + 1] - o[q] : 0;
-        } else if (base + q < n) {
-            r += 1;
+// The workgroup copies elements [d, d + m) of one column from [s, s + m).
+template <int E>
+__device__ __forceinline__ void copy_piece(const char *__restrict__ in, char *__restrict__ out, bool vec,
+                                           int64_t d, int64_t s, int64_t m) {
+    using T = typename Elem<E>::T;
+    const T *src = reinterpret_cast<const T *>(in);
+    T *dst = reinterpret_cast<T *>(out);
+    const int t = threadIdx.x;
+    const int64_t delta = s - d;
+    if (E >= 4 && vec) {
+        constexpr int VE = 16 / E;
+        const int64_t e = d + m;
+        const int64_t a0 = (d + VE - 1) / VE * VE, a1 = e / VE * VE;
+        if (a0 < a1) {
+            if (t < a0 - d) dst[d + t] = src[d + t + delta];
+            if (t < e - a1) dst[a1 + t] = src[a1 + t + delta];
+            for (int64_t v = a0 / VE + t; v < a1 / VE; v += kPT)
+                store_nt(reinterpret_cast<uint4 *>(dst + v * VE), load_a4(src + v * VE + delta));
+            return;
         }
     }
-    uint32_t tot_keep, tot_rej;
-    int64_t tot_len;
-    uint32_t rank = block_excl_sum_u32<kNW>(c, tot_keep, wcnt);
-    int64_t dst = block_excl_sum_i64<kNW>(l, tot_len, wlen);
-    uint32_t rpos = reject_ids ? block_excl_sum_u32<kNW>(r, tot_rej, wrej) : 0u;
+    for (int64_t p = d + t; p < d + m; p += kPT) dst[p] = src[p + delta];
+}
+
+__global__ __launch_bounds__(kPT) void compact_piece_kernel(
+    const int64_t *__restrict__ off, int64_t n, int64_t NT, const uint8_t *__restrict__ keep,
+    PieceParts parts, int64_t nb, CompactCols cols, int n_cols, int64_t *__restrict__ offsets_out,
+    int32_t *__restrict__ kept_ids, int64_t *__restrict__ n_kept_tokens, int32_t *__restrict__ reject_ids,
+    int64_t budget) {
+    __shared__ uint32_t w_cnt[kPW], w_pcs[kPW];
+    __shared__ int64_t w_len[kPW];
+    __shared__ int64_t sel[3];
+    __shared__ int64_t piece[3];
+    const int t = threadIdx.x;
+    const int64_t q = blockIdx.x;
+    if (t == 0) {
+        sel[0] = sel[1] = sel[2] = 0;
+        piece[0] = piece[1] = piece[2] = 0;   // an unmatched piece copies nothing
+    }
+
+    // 1. Exclusive prefix of the block partials; thread t holds blocks
+    //    [t * kPartsPerThread, (t + 1) * kPartsPerThread).
+    uint32_t c[kPartsPerThread], pc[kPartsPerThread];
+    int64_t l[kPartsPerThread];
+    uint32_t cs = 0, ps = 0;
+    int64_t ls = 0;
 #pragma unroll
-    for (int q = 0; q < kItems; ++q) {
-        const int64_t i = base + q;
-        if (kp[q]) {
-            const int64_t len = (o[q + 1] > o[q]) ? o[q + 1] - o[q] : 0;
-            kdst[rank] = (int32_t)(dst < NT ? dst : NT);
-            ksrc[rank] = (int32_t)o[q];
-            if (writer) {
+    for (int k = 0; k < kPartsPerThread; ++k) {
+        const int64_t b = (int64_t)t * kPartsPerThread + k;
+        c[k] = b < nb ? (uint32_t)parts.cnt[b] : 0u;
+        l[k] = b < nb ? parts.len[b] : 0;
+        pc[k] = b < nb ? (uint32_t)parts.pcs[b] : 0u;
+        cs += c[k];
+        ls += l[k];
+        ps += pc[k];
+    }
+    uint32_t tot_c, tot_p;
+    int64_t tot_l;
+    uint32_t cb = block_excl_sum_u32<kPW>(cs, tot_c, w_cnt);
+    int64_t lb = block_excl_sum_i64<kPW>(ls, tot_l, w_len);
+    uint32_t pb = block_excl_sum_u32<kPW>(ps, tot_p, w_pcs);
+    if (q == 0 && t == 0) {
+        offsets_out[tot_c] = tot_l;
+        *n_kept_tokens = tot_l;
+    }
+
+    if (q < nb) {
+        // 2a. Index outputs of block q.
+#pragma unroll
+        for (int k = 0; k < kPartsPerThread; ++k) {
+            if ((int64_t)t * kPartsPerThread + k == q) {
+                sel[0] = cb;
+                sel[1] = lb;
+            }
+            cb += c[k];
+            lb += l[k];
+        }
+        __syncthreads();
+        if (t < kWave) {
+            const int64_t i = q * kPieceBlock + t;
+            const bool in = t < kPieceBlock && i < n;
+            int64_t len = 0, lo;
+            bool kept = false;
+            if (in) {
+                const int64_t k = kept_span(off, keep, i, NT, lo);
+                kept = k >= 0;
+                len = kept ? k : 0;
+            }
+            const int64_t rank = sel[0] + (int64_t)__popcll(ballot(kept) & lanes_below());
+            const int64_t dst = sel[1] + (wave_incl_scan_i64(len) - len);
+            if (kept) {
                 offsets_out[rank] = dst;
                 kept_ids[rank] = (int32_t)i;
+            } else if (in && reject_ids) {
+                const int64_t rr = i - rank;       // trajectories before i that were rejected
+                if (rr < budget) reject_ids[rr] = (int32_t)i;
             }
-            ++rank;
-            dst += len;
-        } else if (reject_ids && writer && i < n) {
-            if ((int64_t)rpos < budget) reject_ids[rpos] = (int32_t)i;
-            ++rpos;
         }
+        return;
     }
-    if (threadIdx.x == 0) {
-        kdst[tot_keep] = (int32_t)(tot_len < NT ? tot_len : NT);
-        if (writer) {
-            offsets_out[tot_keep] = tot_len;
-            *n_kept_tokens = tot_len;
+
+    // 2b. Piece pq: its block, then its trajectory within the block.
+    const int64_t pq = q - nb;
+    if (pq >= (int64_t)tot_p) return;
+#pragma unroll
+    for (int k = 0; k < kPartsPerThread; ++k) {
+        const int64_t b = (int64_t)t * kPartsPerThread + k;
+        if (b < nb && pc[k] > 0 && (int64_t)pb <= pq && pq < (int64_t)pb + pc[k]) {
+            sel[0] = b;
+            sel[1] = pb;
+            sel[2] = lb;
+        }
+        pb += pc[k];
+        lb += l[k];
+    }
+    __syncthreads();
+    if (t < kWave) {
+        const int64_t b = sel[0];
+        const int64_t i = b * kPieceBlock + t;
+        int64_t len = 0, lo = 0;
+        if (t < kPieceBlock && i < n) {
+            const int64_t k = kept_span(off, keep, i, NT, lo);
+            len = k > 0 ? k : 0;
+        }
+        const int64_t np = (len + kPieceLen - 1) / kPieceLen;
+        const int64_t np_incl = wave_incl_scan_i64(np);
+        const int64_t len_incl = wave_incl_scan_i64(len);
+        const int64_t qq = pq - sel[1];
+        if (np > 0 && np_incl - np <= qq && qq < np_incl) {
+            const int64_t k = qq - (np_incl - np);
+            piece[0] = sel[2] + (len_incl - len) + k * kPieceLen;
+            piece[1] = lo + k * kPieceLen;
+            piece[2] = (len - k * kPieceLen) < kPieceLen ? len - k * kPieceLen : kPieceLen;
         }
     }
     __syncthreads();
-
-    // 2. Copy: the waves of the grid split the packed batch into equal,
-    //    1024-element-aligned ranges.
-    const int64_t n_kept = tot_keep;
-    const int64_t total = tot_len < NT ? tot_len : NT;
-    if (n_kept == 0 || total == 0 || n_cols == 0) return;
-    const int64_t waves = (int64_t)gridDim.x * kNW;
-    int64_t per = (total + waves - 1) / waves;
-    per = (per + 1023) / 1024 * 1024;
-    const int64_t cs = ((int64_t)blockIdx.x * kNW + threadIdx.x / kWave) * per;
-    if (cs >= total) return;
-    const int64_t ce = (cs + per < total) ? cs + per : total;
-    LdsSpans sp{kdst, ksrc};
-    int64_t j = lds_last_le(kdst, n_kept, cs);
-    while (j + 1 < n_kept && (int64_t)kdst[j + 1] <= cs) ++j;     // skip empty spans
-    for (int col = 0; col < n_cols; ++col) copy_range_col(cols, col, sp, n_kept, NT, cs, ce, j);
+    const int64_t d = piece[0], s = piece[1];
+    int64_t m = piece[2];
+    if (d >= NT || m <= 0) return;          // overlapping (malformed) offsets overflow the output
+    if (d + m > NT) m = NT - d;
+    for (int col = 0; col < n_cols; ++col) {
+        const char *in = (const char *)cols.in[col];
+        char *out = (char *)cols.out[col];
+        const bool vec = cols.vec[col] != 0;
+        switch (cols.elem[col]) {
+            case 1: copy_piece<1>(in, out, vec, d, s, m); break;
+            case 2: copy_piece<2>(in, out, vec, d, s, m); break;
+            case 4: copy_piece<4>(in, out, vec, d, s, m); break;
+            default: copy_piece<8>(in, out, vec, d, s, m); break;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -359,40 +455,46 @@ __global__ __launch_bounds__(256) void compact_copy_kernel(
 int64_t map_capacity(int64_t n_tokens) { return (n_tokens + kCopyChunk - 1) / kCopyChunk + 1; }
 
 CompactWs compact_ws_carve(void *ws, int64_t n, int64_t n_tokens) {
-    (void)n_tokens;
+    const size_t nb = (size_t)piece_blocks(n);
     char *p = (char *)ws;
     CompactWs w;
     w.hdr = (int64_t *)p;          p += 256;
     w.kept_src = (int64_t *)p;     p += align256((size_t)n * 8);
-    w.chunk_first = (int32_t *)p;
+    w.chunk_first = (int32_t *)p;  p += align256((size_t)map_capacity(n_tokens) * 4);
+    w.parts.cnt = (int32_t *)p;    p += align256(nb * 4);
+    w.parts.len = (int64_t *)p;    p += align256(nb * 8);
+    w.parts.pcs = (int32_t *)p;
     return w;
 }
 
 size_t compact_ws_bytes(int64_t n, int64_t n_tokens) {
-    return 256 + align256((size_t)n * 8) + align256((size_t)map_capacity(n_tokens) * 4);
+    const size_t nb = (size_t)piece_blocks(n);
+    return 256 + align256((size_t)n * 8) + align256((size_t)map_capacity(n_tokens) * 4) +
+           align256(nb * 4) * 2 + align256(nb * 8);
 }
 
-bool compact_span_ok(int64_t n, int64_t n_tokens) {
-    return n <= kSpanMaxN && n_tokens < (int64_t)INT32_MAX;
+bool compact_piece_ok(int64_t n, int64_t n_tokens) {
+    return n <= kPieceMaxN && n_tokens / kPieceLen < ((int64_t)1 << 30);
 }
 
-hipError_t launch_compact_span(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
-                               const CompactCols &cols, int n_cols, int64_t *offsets_out,
-                               int32_t *kept_ids, int64_t *n_kept_tokens, int32_t *reject_ids,
-                               int64_t budget, hipStream_t stream) {
-    // One 1024-thread workgroup per CU.
-    unsigned grid = (unsigned)(resident_waves() / 16);
-    if (grid < 1) grid = 1;
-    const int64_t items = (n + kT - 1) / kT;
-#define PACE_SPAN(K)                                                                            \
-    compact_span_kernel<K><<<grid, kT, 0, stream>>>(offsets, n, n_tokens, keep, cols, n_cols,  \
-        offsets_out, kept_ids, n_kept_tokens, reject_ids, budget)
-    if (items <= 1) PACE_SPAN(1);
-    else if (items <= 2) PACE_SPAN(2);
-    else if (items <= 4) PACE_SPAN(4);
-    else PACE_SPAN(8);
-#undef PACE_SPAN
-    return hipGetLastError();
+hipError_t launch_compact_partials(const int64_t *offsets, int64_t n, int64_t n_tokens,
+                                   const uint8_t *keep, const PieceParts &parts, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    return launch(-1, compact_partials_kernel, dim3((unsigned)piece_blocks(n)), dim3(kWave), stream,
+                  offsets, n, n_tokens, keep, parts);
+}
+
+hipError_t launch_compact_pieces(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
+                                 const PieceParts &parts, const CompactCols &cols, int n_cols,
+                                 int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
+                                 int32_t *reject_ids, int64_t budget, hipStream_t stream) {
+    // Block workgroups, then at most n + n_tokens / kPieceLen piece workgroups
+    // (a span of len tokens has at most len / kPieceLen + 1 pieces).
+    const int64_t nb = piece_blocks(n);
+    const int64_t grid = (nb > 0 ? nb : 1) + n + n_tokens / kPieceLen + 1;
+    return launch(kPhaseCompact, compact_piece_kernel, dim3((unsigned)grid), dim3(kPT), stream, offsets, n,
+                  n_tokens, keep, parts, nb, cols, n_cols, offsets_out, kept_ids, n_kept_tokens,
+                  reject_ids, budget);
 }
 
 hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_tokens,
@@ -403,17 +505,20 @@ hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_to
     if (blocks > 1024) blocks = 1024;
     if (blocks < 1) blocks = 1;
     dim3 grid((unsigned)blocks, (unsigned)n_cols);
-    compact_copy_kernel<<<grid, 256, 0, stream>>>(cols, offsets_out, w.kept_src, w.chunk_first, w.hdr, n_tokens);
-    return hipGetLastError();
+    return launch(kPhaseCompact, compact_copy_kernel, grid, dim3(256), stream, cols, offsets_out,
+                  w.kept_src, w.chunk_first, w.hdr, n_tokens);
 }
 
 hipError_t launch_compact(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                           const CompactCols &cols, int n_cols, int64_t *offsets_out,
                           int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, hipStream_t stream) {
-    if (compact_span_ok(n, n_tokens))
-        return launch_compact_span(offsets, n, n_tokens, keep, cols, n_cols, offsets_out, kept_ids,
-                                   n_kept_tokens, nullptr, 0, stream);
     CompactWs w = compact_ws_carve(ws, n, n_tokens);
+    if (compact_piece_ok(n, n_tokens)) {
+        hipError_t e = launch_compact_partials(offsets, n, n_tokens, keep, w.parts, stream);
+        if (e != hipSuccess) return e;
+        return launch_compact_pieces(offsets, n, n_tokens, keep, w.parts, cols, n_cols, offsets_out,
+                                     kept_ids, n_kept_tokens, nullptr, 0, stream);
+    }
     compact_scan_kernel<<<1, kT, 0, stream>>>(offsets, n, n_tokens, keep, offsets_out, kept_ids,
                                              n_kept_tokens, w.kept_src, w.chunk_first,
                                              map_capacity(n_tokens), w.hdr);

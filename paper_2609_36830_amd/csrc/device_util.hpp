@@ -155,6 +155,12 @@ __device__ __forceinline__ uint4 load_nt(const uint4 *p) {
     const pace_v4u x = __builtin_nontemporal_load(reinterpret_cast<const pace_v4u *>(p));
     return make_uint4(x.x, x.y, x.z, x.w);
 }
+// 16 bytes from an address that is only 4-byte aligned (one dwordx4 load).
+typedef unsigned pace_v4u_a4 __attribute__((ext_vector_type(4), aligned(4)));
+__device__ __forceinline__ uint4 load_a4(const void *p) {
+    const pace_v4u_a4 x = *reinterpret_cast<const pace_v4u_a4 *>(p);
+    return make_uint4(x.x, x.y, x.z, x.w);
+}
 __device__ __forceinline__ void store_nt(uint4 *p, const uint4 &v) {
     const pace_v4u x = {v.x, v.y, v.z, v.w};
     __builtin_nontemporal_store(x, reinterpret_cast<pace_v4u *>(p));

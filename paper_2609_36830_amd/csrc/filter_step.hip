@@ -3,15 +3,16 @@
 //
 //   1. score_reduce   (score.hip)    every tag read once, per-chunk pieces
 //   2. score_finalize (score.hip)    one thread per trajectory: the score
-//   3. rank           (select.hip)   exact rank by counting -> keep flags
-//   4. compact_span   (compact.hip)  every workgroup rebuilds the kept-span
-//                                    scan in LDS, then copies its share of
-//                                    the batch; workgroup 0 writes the packed
-//                                    offsets, kept ids and rejected ids
+//   3. rank           (select.hip)   exact rank by counting -> keep flags,
+//                                    plus per-block kept counts, kept tokens
+//                                    and piece counts
+//   4. compact_piece  (compact.hip)  one workgroup per block writes the packed
+//                                    offsets, kept ids and rejected ids; one
+//                                    per piece of a kept span copies it
 //
 // The same results as pace_score, pace_budget, pace_select and pace_compact
 // called in sequence, in four launches instead of six. Pools beyond the
-// rank and span limits use those calls' kernels.
+// rank and piece limits use those calls' kernels.
 #include "device_util.hpp"
 #include "kernels.hpp"
 
@@ -43,11 +44,12 @@ hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64
     e = launch_score_finalize(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix,
                               w_wait, gamma, chunk_len, score, gen_sum, gen_count, sws, stream);
     if (e != hipSuccess) return e;
-    if (n <= kRankMaxN && compact_span_ok(n, n_tokens)) {
-        e = launch_rank(score, n, budget, keep, stream);
+    if (n <= kRankMaxN && compact_piece_ok(n, n_tokens)) {
+        const CompactWs cw = compact_ws_carve(cws_base, n, n_tokens);
+        e = launch_rank(score, n, budget, keep, offsets, n_tokens, cw.parts, stream);
         if (e != hipSuccess) return e;
-        return launch_compact_span(offsets, n, n_tokens, keep, cols, n_cols, offsets_out, kept_ids,
-                                   n_kept_tokens, reject_ids, budget, stream);
+        return launch_compact_pieces(offsets, n, n_tokens, keep, cw.parts, cols, n_cols, offsets_out,
+                                     kept_ids, n_kept_tokens, reject_ids, budget, stream);
     }
     e = launch_select(score, n, budget, keep, reject_ids, sel_ws, stream);
     if (e != hipSuccess) return e;

@@ -2,14 +2,43 @@
 // kernels. Not part of the public ABI.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
+
+#include <tuple>
 
 namespace pace {
 
 // Waves the device keeps resident for the streaming kernels (CUs x 16).
 int64_t resident_waves();
+
+// ---- launches with optional per-kernel timing ------------------------------
+// The phases a caller may time (pace_time_next_kernel). When a timer is armed
+// for a phase on the calling host thread, that phase's next kernel is
+// launched with hipExtLaunchKernel and the two events, which then bracket
+// the kernel's own execution; the timer is consumed by that launch.
+enum TimedPhase : int { kPhaseReduce = 0, kPhaseFinalize = 1, kPhaseSelect = 2, kPhaseCompact = 3,
+                        kPhaseCount = 4 };
+bool take_phase_timer(int phase, hipEvent_t *start, hipEvent_t *stop);
+
+template <typename... P, typename... A>
+hipError_t launch(int phase, void (*kernel)(P...), dim3 grid, dim3 block, hipStream_t stream, A... a) {
+    static_assert(sizeof...(P) == sizeof...(A), "kernel argument count");
+    hipEvent_t t0 = nullptr, t1 = nullptr;
+    if (phase >= 0 && take_phase_timer(phase, &t0, &t1)) {
+        std::tuple<P...> held{static_cast<P>(a)...};
+        void *argv[sizeof...(P)];
+        std::apply([&argv](auto &...x) {
+            int k = 0;
+            ((argv[k++] = (void *)&x), ...);
+        }, held);
+        return hipExtLaunchKernel((const void *)kernel, grid, block, argv, 0, stream, t0, t1, 0);
+    }
+    kernel<<<grid, block, 0, stream>>>(static_cast<P>(a)...);
+    return hipGetLastError();
+}
 
 // ---- score: segmented reduction over token chunks --------------------------
 // One wave reduces one chunk of consecutive tokens; the chunk length is a
@@ -59,8 +88,24 @@ constexpr int kSelectMaxItems = 16;   // keys held in registers per thread
 // Pools up to this size are selected by the multi-workgroup rank-by-counting
 // kernel; larger pools by the single-workgroup radix select.
 constexpr int64_t kRankMaxN = 8192;
+// ---- compaction by pieces: block partials ----------------------------------
+// Consecutive trajectories form blocks of kPieceBlock; a kept span of len
+// tokens is cut into ceil(len / kPieceLen) pieces. Per block: kept count,
+// kept tokens and pieces (lengths from offsets clamped to [0, n_tokens]).
+constexpr int kPieceBlock = 16;
+constexpr int64_t kPieceLen = 16384;
+constexpr int64_t kPieceMaxN = 8192;   // at most 512 blocks
+struct PieceParts {
+    int32_t *cnt;
+    int64_t *len;
+    int32_t *pcs;
+};
+inline int64_t piece_blocks(int64_t n) { return (n + kPieceBlock - 1) / kPieceBlock; }
+
 // keep[i] <- 0 for the `budget` first trajectories in (score desc, id asc).
+// With parts.cnt non-null, also writes the block partials of the keep flags.
 hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,
+                       const int64_t *offsets, int64_t n_tokens, const PieceParts &parts,
                        hipStream_t stream);
 size_t select_ws_bytes(int64_t n);
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
@@ -82,22 +127,25 @@ struct CompactWs {
     int64_t *hdr;          // [0] kept trajectories, [1] min(kept tokens, n_tokens)
     int64_t *kept_src;     // [n] source start of each kept span
     int32_t *chunk_first;  // [map_capacity] kept span covering each output chunk's first element
+    PieceParts parts;      // [piece_blocks(n)] block partials (piece path)
 };
 int64_t map_capacity(int64_t n_tokens);
 CompactWs compact_ws_carve(void *ws, int64_t n, int64_t n_tokens);
 size_t compact_ws_bytes(int64_t n, int64_t n_tokens);
 hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_tokens,
                                const int64_t *offsets_out, const CompactWs &w, hipStream_t stream);
-// Single-kernel compaction (scan rebuilt in every workgroup) for pools of at
-// most kSpanMaxN trajectories and fewer than 2^31 tokens. reject_ids may be
-// NULL; when given, the ids with keep == 0 go there in ascending order
-// (at most `budget` of them).
-constexpr int64_t kSpanMaxN = 8192;
-bool compact_span_ok(int64_t n, int64_t n_tokens);
-hipError_t launch_compact_span(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
-                               const CompactCols &cols, int n_cols, int64_t *offsets_out,
-                               int32_t *kept_ids, int64_t *n_kept_tokens, int32_t *reject_ids,
-                               int64_t budget, hipStream_t stream);
+// Piece path (at most kPieceMaxN trajectories): one workgroup per block
+// writes that block's packed offsets, kept ids and rejected ids; one
+// workgroup per piece copies it. reject_ids may be NULL; when given, the ids
+// with keep == 0 go there in ascending order (at most `budget` of them).
+// The block partials come from the rank kernel or from launch_compact_partials.
+bool compact_piece_ok(int64_t n, int64_t n_tokens);
+hipError_t launch_compact_partials(const int64_t *offsets, int64_t n, int64_t n_tokens,
+                                   const uint8_t *keep, const PieceParts &parts, hipStream_t stream);
+hipError_t launch_compact_pieces(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
+                                 const PieceParts &parts, const CompactCols &cols, int n_cols,
+                                 int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
+                                 int32_t *reject_ids, int64_t budget, hipStream_t stream);
 hipError_t launch_compact(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                           const CompactCols &cols, int n_cols, int64_t *offsets_out,
                           int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, hipStream_t stream);

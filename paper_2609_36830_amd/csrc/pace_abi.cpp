@@ -58,6 +58,19 @@ int64_t resident_waves() {
     return (int64_t)cu * 16;
 }
 
+namespace {
+// Armed timers, per host thread: [phase][start, stop].
+thread_local hipEvent_t g_phase_timer[kPhaseCount][2];
+}  // namespace
+
+bool take_phase_timer(int phase, hipEvent_t *start, hipEvent_t *stop) {
+    if (phase < 0 || phase >= kPhaseCount || g_phase_timer[phase][0] == nullptr) return false;
+    *start = g_phase_timer[phase][0];
+    *stop = g_phase_timer[phase][1];
+    g_phase_timer[phase][0] = g_phase_timer[phase][1] = nullptr;
+    return true;
+}
+
 }  // namespace pace
 
 extern "C" {
@@ -259,6 +272,16 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
     if (rc != PACE_OK) return rc;
     *r_hat_inout = r_hat;
     *budget_out = budget;
+    return PACE_OK;
+}
+
+static_assert(PACE_PHASE_COUNT == kPhaseCount, "phase count");
+
+int pace_time_next_kernel(int phase, void *start_event, void *stop_event) {
+    if (phase < 0 || phase >= PACE_PHASE_COUNT) return PACE_ERR_INVALID_ARG;
+    if ((start_event == nullptr) != (stop_event == nullptr)) return PACE_ERR_INVALID_ARG;
+    g_phase_timer[phase][0] = (hipEvent_t)start_event;
+    g_phase_timer[phase][1] = (hipEvent_t)stop_event;
     return PACE_OK;
 }
 

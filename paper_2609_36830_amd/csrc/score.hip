@@ -264,15 +264,15 @@ hipError_t launch_score_reduce(const int32_t *tags, const int64_t *offsets, int6
     if (n == 0 || ch == 0) return hipSuccess;
     const unsigned grid = (unsigned)((ch + kWavesPerBlock - 1) / kWavesPerBlock);
     const bool narrow = (int64_t)V < (1 << 24) - 1;
-#define PACE_REDUCE(NARROW, VEC)                                                              \
-    score_reduce_kernel<NARROW, VEC><<<grid, 256, 0, stream>>>(tags, offsets, n, n_tokens,   \
-        chunk_len, ch, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt)
+#define PACE_REDUCE(NARROW, VEC)                                                            \
+    return launch(kPhaseReduce, score_reduce_kernel<NARROW, VEC>, dim3(grid), dim3(256), stream, \
+                  tags, offsets, n, n_tokens, chunk_len, ch, ws.part_sum, ws.part_cnt,         \
+                  ws.carry_sum, ws.carry_cnt)
     if (narrow && vec_ok) PACE_REDUCE(true, true);
-    else if (narrow) PACE_REDUCE(true, false);
-    else if (vec_ok) PACE_REDUCE(false, true);
-    else PACE_REDUCE(false, false);
+    if (narrow) PACE_REDUCE(true, false);
+    if (vec_ok) PACE_REDUCE(false, true);
+    PACE_REDUCE(false, false);
 #undef PACE_REDUCE
-    return hipGetLastError();
 }
 
 hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_tokens,
@@ -283,10 +283,12 @@ hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_to
     if (n == 0) return hipSuccess;
     const unsigned grid = (unsigned)((n + 255) / 256);
     if (use_prefix && W <= kWindowLdsMax)
-        score_finalize_kernel<true><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, 1, w_wait, gamma, chunk_len, ws, score, gen_sum, gen_count);
-    else
-        score_finalize_kernel<false><<<grid, 256, 0, stream>>>(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, chunk_len, ws, score, gen_sum, gen_count);
-    return hipGetLastError();
+        return launch(kPhaseFinalize, score_finalize_kernel<true>, dim3(grid), dim3(256), stream, offsets,
+                      n, n_tokens, completion, V, prefix, window, W, 1, w_wait, gamma, chunk_len, ws,
+                      score, gen_sum, gen_count);
+    return launch(kPhaseFinalize, score_finalize_kernel<false>, dim3(grid), dim3(256), stream, offsets, n,
+                  n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma,
+                  chunk_len, ws, score, gen_sum, gen_count);
 }
 
 hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,

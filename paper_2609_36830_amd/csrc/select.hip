@@ -204,14 +204,24 @@ constexpr int kRankQ = 16;
 constexpr int kRankS = kRankT / kRankQ;
 constexpr int kRankTile = 4096;
 
+static_assert(kRankQ == kPieceBlock, "a rank workgroup covers one partials block");
+
 __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__ score, int64_t n,
-                                                     int64_t budget, uint8_t *__restrict__ keep) {
+                                                     int64_t budget, uint8_t *__restrict__ keep,
+                                                     const int64_t *__restrict__ off, int64_t NT,
+                                                     PieceParts parts) {
     __shared__ uint64_t tile[kRankTile];
     __shared__ uint32_t part[kRankS][kRankQ + 1];
     const int t = threadIdx.x;
     const int q = t % kRankQ, s = t / kRankQ;
     const int32_t i = (int32_t)((int64_t)blockIdx.x * kRankQ + q);
     const uint64_t ki = score_key(i < n ? score[i] : 0.0);
+    // Span length of this workgroup's trajectories, for the block partials.
+    int64_t span = 0;
+    if (parts.cnt && t < kRankQ && i < n) {
+        const int64_t lo = clamp64(off[i], 0, NT), hi = clamp64(off[i + 1], 0, NT);
+        span = hi > lo ? hi - lo : 0;
+    }
     uint32_t cnt = 0;
     for (int64_t b0 = 0; b0 < n; b0 += kRankTile) {
         const int m = (int)((n - b0) < kRankTile ? (n - b0) : kRankTile);
@@ -235,12 +245,25 @@ __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__
     }
     part[s][q] = cnt;
     __syncthreads();
-    if (t < kRankQ) {
+    if (t < kWave) {   // wave 0; lanes below kRankQ own the targets
         const int64_t ii = (int64_t)blockIdx.x * kRankQ + t;
-        if (ii < n) {
+        bool kept = false;
+        if (t < kRankQ && ii < n) {
             uint32_t r = 0;
             for (int k = 0; k < kRankS; ++k) r += part[k][t];
-            keep[ii] = ((int64_t)r < budget) ? 0 : 1;
+            kept = (int64_t)r >= budget;
+            keep[ii] = kept ? 1 : 0;
+        }
+        if (parts.cnt) {
+            const int64_t len = kept ? span : 0;
+            const uint32_t c = (uint32_t)__popcll(ballot(kept));
+            const int64_t l = wave_sum_i64(len);
+            const int64_t pc = wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
+            if (t == 0) {
+                parts.cnt[blockIdx.x] = (int32_t)c;
+                parts.len[blockIdx.x] = l;
+                parts.pcs[blockIdx.x] = (int32_t)pc;
+            }
         }
     }
 }
@@ -276,10 +299,11 @@ size_t select_ws_bytes(int64_t n) {
 }
 
 hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,
+                       const int64_t *offsets, int64_t n_tokens, const PieceParts &parts,
                        hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    rank_kernel<<<(unsigned)((n + kRankQ - 1) / kRankQ), kRankT, 0, stream>>>(score, n, budget, keep);
-    return hipGetLastError();
+    return launch(kPhaseSelect, rank_kernel, dim3((unsigned)((n + kRankQ - 1) / kRankQ)), dim3(kRankT),
+                  stream, score, n, budget, keep, offsets, n_tokens, parts);
 }
 
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
@@ -287,7 +311,8 @@ hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t
     if (n == 0) return hipSuccess;
     const int64_t items = (n + kT - 1) / kT;
     if (n <= kRankMaxN) {
-        hipError_t e = launch_rank(score, n, budget, keep, stream);
+        hipError_t e = launch_rank(score, n, budget, keep, nullptr, 0, PieceParts{nullptr, nullptr, nullptr},
+                                   stream);
         if (e != hipSuccess || budget == 0) return e;
         if (items <= 1)
             emit_rejects_kernel<1><<<1, kT, 0, stream>>>(keep, n, budget, reject_ids);
@@ -300,10 +325,10 @@ hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t
         return hipGetLastError();
     }
     if (items <= 16)
-        select_reg_kernel<16><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids);
-    else
-        select_strided_kernel<0><<<1, kT, 0, stream>>>(score, n, budget, keep, reject_ids, (uint64_t *)ws);
-    return hipGetLastError();
+        return launch(kPhaseSelect, select_reg_kernel<16>, dim3(1), dim3(kT), stream, score, n, budget,
+                      keep, reject_ids);
+    return launch(kPhaseSelect, select_strided_kernel<0>, dim3(1), dim3(kT), stream, score, n, budget,
+                  keep, reject_ids, (uint64_t *)ws);
 }
 
 }  // namespace pace

@@ -165,3 +165,14 @@ def test_select_and_compact_host_argument_errors(L):
     assert L.pace_compact(None, 10, 100, FAKE, 1, cols, ok_e, cols, FAKE, FAKE, FAKE, FAKE, 1 << 20, None) == -1
     assert L.pace_compact(FAKE, 10, 100, FAKE, 1, cols, ok_e, cols, FAKE, FAKE, FAKE, FAKE, 8, None) == -2
     assert L.pace_validate(FAKE, None, 10, 100, FAKE, 5, None, 0, FAKE, None) == -1
+
+
+def test_time_next_kernel_arguments(L):
+    assert L.pace_time_next_kernel(-1, None, None) == -1
+    assert L.pace_time_next_kernel(4, None, None) == -1
+    assert L.pace_time_next_kernel(0, FAKE, None) == -1
+    assert L.pace_time_next_kernel(0, None, FAKE) == -1
+    # arm then disarm: nothing is launched, so the fake handles are never used
+    assert L.pace_time_next_kernel(3, FAKE, FAKE) == 0
+    for phase in range(4):
+        assert L.pace_time_next_kernel(phase, None, None) == 0
