@@ -45,6 +45,40 @@ def parse():
     return ap.parse_args()
 
 
+PHASES = ("score_reduce", "score_finalize", "rank", "compact_piece")
+
+
+def reduce_bytes(pool, cus):
+    """Algorithmic bytes of one score_reduce launch: 4 B per tag read, 8 B per
+    offset read, 16 B per trajectory (piece sum and count written) and 16 B
+    per token chunk (carry written); one chunk per resident wave (CUs x 16),
+    2048-token aligned."""
+    waves = cus * 16
+    chunk = max(2048, -(-(-(-pool.n_tokens // waves)) // 2048) * 2048)
+    chunks = -(-pool.n_tokens // chunk)
+    return 4 * pool.n_tokens + 8 * (pool.n + 1) + 16 * pool.n + 16 * chunks
+
+
+def reduce_traffic(config):
+    """HBM bytes per score_reduce launch measured with rocprofv3 counters
+    (FETCH_SIZE x 2.0 + WRITE_SIZE x 1.0, the factors a plain device copy of
+    known size gives), or None when the kernel's sources have changed since
+    the counters were taken."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("score.hip", "score_math.hpp", "device_util.hpp"):
+        with open(os.path.join(ROOT, "paper_2609_36830_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    rec = REDUCE_COUNTERS.get(config)
+    if rec is None or rec["sha256"] != h.hexdigest():
+        return None
+    return rec["bytes"]
+
+
+# config -> {"sha256": digest of the score_reduce sources, "bytes": HBM bytes per launch}
+REDUCE_COUNTERS = {}
+
+
 def alg_bytes(pool, n_keep_tok, col_bytes, W):
     """Algorithmic bytes of one step: every tag read once, every kept token of
     each payload column read and written once, plus the per-trajectory arrays
@@ -152,6 +186,25 @@ def main():
     per_compact = np.array([e[2].elapsed_time(e[3]) for e in cev])
     assert int(step.n_kept_tokens.item()) == n_keep_tok
 
+    # Per-kernel durations: K more cold steps, each phase's kernel launched
+    # with its own HIP event pair (hipExtLaunchKernel), so each pair times
+    # that kernel's execution on the stream it runs on.
+    def ev_pair():
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        b.record(stream)
+        return a, b
+    kev = [[ev_pair() for _ in PHASES] for _ in range(K)]
+    torch.cuda.synchronize()
+    for k in range(K):
+        flush.max()
+        for ph in range(len(PHASES)):
+            pace.pace_time_next_kernel(ph, *kev[k][ph])
+        fused_step()
+    torch.cuda.synchronize()
+    kernel_us = {name: np.array([kev[k][ph][0].elapsed_time(kev[k][ph][1]) * 1e3 for k in range(K)])
+                 for ph, name in enumerate(PHASES)}
+
     # Warm back-to-back steps (no flush) for context.
     warm_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
@@ -173,6 +226,8 @@ def main():
     ms = float(per_step.mean())
     B, B_score = alg_bytes(pool, n_keep_tok, [c.element_size() for c in cols], W)
     score_ms = float(per_score.mean())
+    B_red = reduce_bytes(pool, torch.cuda.get_device_properties(dev).multi_processor_count)
+    red_s = float(kernel_us["score_reduce"].mean()) * 1e-6
     out = {
         "metric": METRIC,
         "value": pool.n_tokens / (ms * 1e-3),
@@ -203,16 +258,19 @@ def main():
         "separate_calls_ms_per_step": float(calls_step_ms.mean()),
         "per_call_ms": {"pace_score": score_ms, "pace_budget+pace_select": float(per_select.mean()),
                         "pace_compact": float(per_compact.mean())},
+        "kernel_us_mean": {k: float(v.mean()) for k, v in kernel_us.items()},
+        "kernel_us_p50": {k: float(np.median(v)) for k, v in kernel_us.items()},
         "warm_ms_per_step": warm_ms,
         "wall_s_timed_region": wall,
         "roofline": {
-            "kernel": "pace_score (score_reduce + score_finalize)",
+            "kernel": "score_reduce",
             "bound": "hbm",
-            "achieved": B_score / (score_ms * 1e-3) / 1e9,
+            "achieved": B_red / red_s / 1e9,
             "peak": HBM_PEAK / 1e9,
             "unit": "GB/s",
-            "frac": B_score / (score_ms * 1e-3) / HBM_PEAK,
-            "traffic": None,
+            "frac": B_red / red_s / HBM_PEAK,
+            "traffic": reduce_traffic(args.config),
+            "alg_bytes": B_red,
         },
     }
     if not args.no_cpu_baseline:

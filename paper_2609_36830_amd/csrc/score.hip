@@ -33,10 +33,10 @@ namespace {
 
 constexpr int kVec = 4;                       // tags per lane per window
 constexpr int kWin = kWave * kVec;            // 256 tokens per wave window
-constexpr int kUnroll = 8;                    // windows in flight per wave
-constexpr int kSuper = kWin * kUnroll;        // 2048
+constexpr int kUnroll = 4;                    // windows per super-window
+constexpr bool kDoubleBuffer = false;         // two super-windows in flight
 constexpr int kWavesPerBlock = 4;
-static_assert(kScoreChunkAlign % kSuper == 0, "chunk must be a multiple of the super-window");
+static_assert(kScoreChunkAlign % (kWin * kUnroll) == 0, "chunk must be a multiple of the super-window");
 
 // Lane k caches clamp(off[base + k], 0, NT); reads of increasing indices only.
 struct BoundCache {
@@ -67,26 +67,26 @@ __device__ __forceinline__ void add_all_wide(const int4 &v, uint64_t &s, uint32_
     c += (u0 != 0u) + (u1 != 0u) + (u2 != 0u) + (u3 != 0u);
 }
 
-// Elements of this lane's vector whose positions lie in [lo, hi).
-__device__ __forceinline__ void add_range(const int4 &v, int64_t p0, int64_t lo, int64_t hi,
+// Elements of this lane's vector (relative positions r0 .. r0 + 3) that lie
+// in [rlo, rlo + rlen).
+__device__ __forceinline__ void add_range(const int4 &v, uint32_t r0, uint32_t rlo, uint32_t rlen,
                                           uint64_t &s, uint32_t &c) {
     const int x[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        int64_t p = p0 + e;
-        if (p >= lo && p < hi) {
-            uint32_t u = (uint32_t)x[e] + 1u;
+        if (r0 + (uint32_t)e - rlo < rlen) {
+            const uint32_t u = (uint32_t)x[e] + 1u;
             s += u;
             c += (u != 0u);
         }
     }
 }
 
-template <bool kVecLoad>
+template <bool kVecLoad, int U>
 __device__ __forceinline__ void load_super(const int32_t *__restrict__ tags, int64_t pos, int64_t ce,
-                                           int lane, int4 (&v)[kUnroll]) {
+                                           int lane, int4 (&v)[U]) {
 #pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
+    for (int k = 0; k < U; ++k) {
         const int64_t q = pos + (int64_t)k * kWin + (int64_t)lane * kVec;
         if (kVecLoad && q + kVec <= ce) {
             v[k] = *reinterpret_cast<const int4 *>(tags + q);
@@ -102,7 +102,7 @@ __device__ __forceinline__ void load_super(const int32_t *__restrict__ tags, int
 
 // kNarrow: every tag + 1 < 2^24, so a lane's 32 tags of one super-window sum
 // below 2^29 in 32 bits before widening.
-template <bool kNarrow, bool kVecLoad>
+template <bool kNarrow, bool kVecLoad, int U = kUnroll, bool kDouble = kDoubleBuffer>
 __global__ __launch_bounds__(256) void score_reduce_kernel(
     const int32_t *__restrict__ tags, const int64_t *__restrict__ off, int64_t n, int64_t NT,
     int64_t chunk_len, int64_t n_chunks, uint64_t *__restrict__ part_sum,
@@ -114,28 +114,52 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
     const int64_t cs = chunk * chunk_len;
     const int64_t ce = (cs + chunk_len < NT) ? cs + chunk_len : NT;
 
-    // The first super-window's loads do not depend on the trajectory search:
-    // issue them first so the search latency hides under them.
-    int4 v[kUnroll];
-    load_super<kVecLoad>(tags, cs, ce, lane, v);
+    // The first super-window's loads (the first two, double-buffered) do not
+    // depend on the trajectory search: issue them first so the search latency
+    // hides under them. Double-buffered, the next super-window is in flight
+    // while one is summed.
+    constexpr int64_t kSuper = (int64_t)kWin * U;
+    int4 va[U], vb[kDouble ? U : 1];
+    load_super<kVecLoad>(tags, cs, ce, lane, va);
+    if (kDouble && cs + kSuper < ce) load_super<kVecLoad>(tags, cs + kSuper, ce, lane, vb);
 
-    // Trajectory that contains the chunk's first token.
-    const int64_t s = wave_last_le(off, n, cs);
+    // Trajectory that contains the chunk's first token. First guess: the
+    // 64 offsets around the position the token would have if all
+    // trajectories were equally long (one round of loads, which also fills
+    // the bound cache); if the answer is not inside that window, a 64-ary
+    // search over all offsets.
     BoundCache bc;
+    int64_t s;
+    {
+        const int64_t guess = NT > 0 ? (int64_t)((double)cs / (double)NT * (double)n) : 0;
+        const int64_t top = (n + 1 > kWave) ? n + 1 - kWave : 0;
+        const int64_t base = guess - kWave / 2 < 0 ? 0 : (guess - kWave / 2 > top ? top : guess - kWave / 2);
+        const int64_t idx = base + lane;
+        const int64_t raw = (idx <= n) ? off[idx] : INT64_MAX;
+        const uint64_t m = ballot(idx <= n && raw <= cs);
+        const bool lo_ok = base == 0 || (m & 1ull);
+        const bool hi_ok = base + kWave > n || !(m >> (kWave - 1));
+        if (lo_ok && hi_ok) {
+            s = base + (int64_t)__popcll(m) - 1;
+            bc.base = base;
+            bc.val = (idx <= n) ? clamp64(raw, 0, NT) : NT;
+        } else {
+            s = wave_last_le(off, n, cs);
+            bc.base = INT64_MIN / 2;          // empty: the first get() loads
+            bc.val = 0;
+        }
+    }
     int64_t cur, cur_end;
     bool valid = false, pending = false, carry_piece = false;
     if (s < 0) {                 // only for malformed offsets: tokens before offsets[0]
         cur = -1;
-        bc.load(off, n, NT, 0);
-        cur_end = readlane_i64(bc.val, 0);
+        cur_end = bc.get(off, n, NT, 0);
     } else if (s >= n) {         // tokens at or past offsets[n]
         cur = n;
-        bc.load(off, n, NT, n);
         cur_end = INT64_MAX;
     } else {
         cur = s;
-        bc.load(off, n, NT, s);
-        const int64_t cur_start = readlane_i64(bc.val, 0);
+        const int64_t cur_start = bc.get(off, n, NT, s);
         cur_end = bc.get(off, n, NT, s + 1);
         valid = true;
         pending = true;
@@ -161,51 +185,76 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
         acc_c = 0;
     };
 
-    for (int64_t pos = cs; pos < ce; pos += kSuper) {
-        if (pos != cs) load_super<kVecLoad>(tags, pos, ce, lane, v);
+    // Adds the super-window at `pos` (held in v) to the running pieces.
+    auto process = [&](int4 (&v)[U], int64_t pos) {
         const int64_t send = (pos + kSuper < ce) ? pos + kSuper : ce;
         if (valid && cur_end >= send) {
             // Fast path: the whole super-window lies in trajectory `cur`.
             if (kNarrow) {
                 uint32_t s32 = 0, c32 = 0;
 #pragma unroll
-                for (int k = 0; k < kUnroll; ++k) add_all(v[k], s32, c32);
+                for (int k = 0; k < U; ++k) add_all(v[k], s32, c32);
                 acc_s += s32;
                 acc_c += c32;
             } else {
 #pragma unroll
-                for (int k = 0; k < kUnroll; ++k) add_all_wide(v[k], acc_s, acc_c);
+                for (int k = 0; k < U; ++k) add_all_wide(v[k], acc_s, acc_c);
             }
-            continue;
+            return;
         }
-        // Boundary path: walk trajectory ends window by window.
+        // Boundary path: the super-window holds trajectory ends. Walk them
+        // in order; for each trajectory piece every lane adds its tags whose
+        // positions fall in the piece.
+        int64_t lo = pos;
+        while (true) {
+            const int64_t hi = cur_end < send ? cur_end : send;
+            if (valid && hi > lo) {
+                // Keep the per-tag work inside this loop: hoisted out of it,
+                // it would hold every tag's (tag + 1) live at once.
 #pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int64_t w = pos + (int64_t)k * kWin;
-            if (w >= ce) break;
-            const int64_t we = (w + kWin < ce) ? w + kWin : ce;
-            const int64_t p0 = w + (int64_t)lane * kVec;
-            int64_t lo = w;
-            while (true) {
-                const int64_t hi = cur_end < we ? cur_end : we;
-                if (valid && hi > lo) add_range(v[k], p0, lo, hi, acc_s, acc_c);
-                if (cur_end > we) break;          // trajectory continues past this window
-                if (pending) flush();             // trajectory `cur` ends at cur_end
-                lo = cur_end;
-                ++cur;
-                while (cur < n && bc.get(off, n, NT, cur + 1) <= lo) ++cur;   // skip empty ones
-                carry_piece = false;
-                if (cur >= n) {
-                    valid = false;
-                    pending = false;
-                    cur_end = INT64_MAX;
-                } else {
-                    valid = true;
-                    cur_end = bc.get(off, n, NT, cur + 1);
-                    pending = lo < ce;
-                }
-                if (lo >= we) break;
+                for (int k = 0; k < U; ++k)
+                    asm volatile("" : "+v"(v[k].x), "+v"(v[k].y), "+v"(v[k].z), "+v"(v[k].w));
+                // Positions relative to the super-window fit in 32 bits.
+                const uint32_t rlo = (uint32_t)(lo - pos), rlen = (uint32_t)(hi - lo);
+                uint64_t ps = 0;
+                uint32_t pc = 0;
+#pragma unroll
+                for (int k = 0; k < U; ++k)
+                    add_range(v[k], (uint32_t)(k * kWin + lane * kVec), rlo, rlen, ps, pc);
+                acc_s += ps;
+                acc_c += pc;
             }
+            if (cur_end > send) break;            // trajectory continues past this super-window
+            if (pending) flush();                 // trajectory `cur` ends at cur_end
+            lo = cur_end;
+            ++cur;
+            while (cur < n && bc.get(off, n, NT, cur + 1) <= lo) ++cur;   // skip empty ones
+            carry_piece = false;
+            if (cur >= n) {
+                valid = false;
+                pending = false;
+                cur_end = INT64_MAX;
+            } else {
+                valid = true;
+                cur_end = bc.get(off, n, NT, cur + 1);
+                pending = lo < ce;
+            }
+            if (lo >= send) break;
+        }
+    };
+
+    if constexpr (kDouble) {
+        for (int64_t pos = cs; pos < ce; pos += 2 * kSuper) {
+            process(va, pos);
+            if (pos + 2 * kSuper < ce) load_super<kVecLoad>(tags, pos + 2 * kSuper, ce, lane, va);
+            if (pos + kSuper >= ce) break;
+            process(vb, pos + kSuper);
+            if (pos + 3 * kSuper < ce) load_super<kVecLoad>(tags, pos + 3 * kSuper, ce, lane, vb);
+        }
+    } else {
+        for (int64_t pos = cs; pos < ce; pos += kSuper) {
+            if (pos != cs) load_super<kVecLoad>(tags, pos, ce, lane, va);
+            process(va, pos);
         }
     }
     if (pending) flush();
