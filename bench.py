@@ -76,7 +76,10 @@ def reduce_traffic(config):
 
 
 # config -> {"sha256": digest of the score_reduce sources, "bytes": HBM bytes per launch}
-REDUCE_COUNTERS = {}
+REDUCE_COUNTERS = {
+    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98115.5 KiB, WRITE_SIZE 273.7 KiB
+    "stress": {"sha256": "7784683db2f83137ed858820ca0f9134061992691cb1499722615668dfae9ce3", "bytes": 201220813},
+}
 
 
 def alg_bytes(pool, n_keep_tok, col_bytes, W):
