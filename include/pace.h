@@ -184,9 +184,9 @@ int pace_validate(const int32_t *tags, const int64_t *offsets, int64_t n_traj, i
  * pace_budget on the host, then pace_score, pace_select and pace_compact on
  * the device, with the same arguments and results as those four calls made
  * in sequence (every output is bit-identical to theirs). The device work is
- * three dependent launches instead of five: the score finalisation, the
- * selection and the ordered scan of kept spans share one workgroup. Pools
- * above 16384 trajectories run the separate kernels.
+ * four dependent launches instead of six: the rank kernel also writes the
+ * per-block partials the compaction needs, and the compaction writes the
+ * rejected ids. Pools above 8192 trajectories run the separate kernels.
  *
  * occupancy, capacity, r_hat_inout, budget_out: as pace_budget ([host]).
  * score_out, gen_sum_out, gen_count_out: as pace_score (gen_* may be NULL).
