@@ -51,7 +51,10 @@ def load_library(path: str):
     lib.oracle_budget.argtypes = [i64, i64, d, d, P, P]
     lib.oracle_select.argtypes = [P, i64, i64, P, P]
     lib.oracle_compact.argtypes = [P, i64, i64, P, ctypes.c_int, P, P, P, P, P, P]
-    for f in ("oracle_validate", "oracle_score", "oracle_budget", "oracle_select", "oracle_compact"):
+    lib.oracle_group_score.argtypes = [P, i64, P, i64, P]
+    lib.oracle_group_expand.argtypes = [P, i64, i64, P, P]
+    for f in ("oracle_validate", "oracle_score", "oracle_budget", "oracle_select", "oracle_compact",
+              "oracle_group_score", "oracle_group_expand"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -175,3 +178,54 @@ def filter_step(pool, mode="effective", w_wait=None, gamma=4, window_min=32,
     return dict(score=sc, S=S, T=T, budget=b, r_hat=r_hat, keep=keep, reject_ids=rej,
                 offsets_out=off_out, kept_ids=ids, packed=packed,
                 n_kept_tokens=int(off_out[-1]))
+
+
+def group_score(score_arr, group_offsets, check=True):
+    """Mean member score per prompt group (empty group: 0)."""
+    s = _c(score_arr, np.float64)
+    go = _c(group_offsets, np.int64)
+    ng = go.shape[0] - 1
+    out = np.empty(max(ng, 1), np.float64)
+    rc = _load().oracle_group_score(_p(s), s.shape[0], _p(go), ng, _p(out))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_group_score")
+        return rc
+    return out[:ng].copy()
+
+
+def group_expand(group_offsets, group_keep, n, check=True):
+    """Trajectory keep flags uint8[n] from group keep flags."""
+    go = _c(group_offsets, np.int64)
+    gk = _c(group_keep, np.uint8)
+    ng = go.shape[0] - 1
+    keep = np.empty(max(int(n), 1), np.uint8)
+    rc = _load().oracle_group_expand(_p(go), ng, int(n), _p(gk), _p(keep))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_group_expand")
+        return rc
+    return keep[: int(n)].copy()
+
+
+def group_filter_step(pool, group_offsets, occupancy, capacity, mode="effective", w_wait=None,
+                      gamma=4, window_min=32, beta=0.0, r_max=0.9, r_hat_prev=0.0, cols=None):
+    """One filter step with prompt groups as the admission unit: trajectory
+    scores, group means, a budget in groups (occupancy and capacity count
+    groups), group selection, and compaction of the kept groups' members."""
+    prefix = None if mode == "raw" else pool.prefix_score
+    window = None if mode == "raw" else pool.window
+    if w_wait is None:
+        w_wait = 0.0 if mode == "gen" else 1.0
+    sc, S, T = score(pool.tags, pool.offsets, pool.completion, pool.V, prefix, window,
+                     w_wait, gamma, window_min)
+    gs = group_score(sc, group_offsets)
+    b, r_hat = budget(occupancy, capacity, r_hat_prev, beta, r_max)
+    gkeep, grej = select(gs, b)
+    keep = group_expand(group_offsets, gkeep, pool.n)
+    cols = [pool.tags] if cols is None else cols
+    off_out, ids, packed = compact(pool.offsets, keep, cols)
+    return dict(score=sc, S=S, T=T, group_score=gs, budget=b, r_hat=r_hat, group_keep=gkeep,
+                reject_group_ids=grej, keep=keep, offsets_out=off_out, kept_ids=ids, packed=packed,
+                n_kept_tokens=int(off_out[-1]))
+

@@ -268,3 +268,59 @@ int oracle_compact(const int64_t *offsets, int64_t n, int64_t n_tokens,
     *n_kept_tokens_out = pos;
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------
+ * Group-level admission (Appendix B: the full method aggregates by the mean
+ * within prompt groups; the score window and the diagnostics count groups).
+ * Consecutive trajectories form prompt groups: group g holds trajectories
+ * [group_offsets[g], group_offsets[g+1]). A group's score is the mean of its
+ * members' scores -- summed in member order, then divided by the member
+ * count -- and an empty group scores 0. Groups are then budgeted, selected
+ * and compacted as whole units: the budget counts groups, and a rejected
+ * group drops all of its members.
+ * ---------------------------------------------------------------------- */
+static int check_groups(const int64_t *group_offsets, int64_t n_groups, int64_t n)
+{
+    if (group_offsets[0] != 0 || group_offsets[n_groups] != n)
+        return ORC_ERR_PRECONDITION;
+    for (int64_t g = 0; g < n_groups; g++)
+        if (group_offsets[g + 1] < group_offsets[g])
+            return ORC_ERR_PRECONDITION;
+    return ORC_OK;
+}
+
+int oracle_group_score(const double *score, int64_t n, const int64_t *group_offsets,
+                       int64_t n_groups, double *group_score_out)
+{
+    if (n < 0 || n_groups < 0 || !group_offsets || (n > 0 && !score) ||
+        (n_groups > 0 && !group_score_out))
+        return ORC_ERR_ARG;
+    int rc = check_groups(group_offsets, n_groups, n);
+    if (rc != ORC_OK)
+        return rc;
+    for (int64_t g = 0; g < n_groups; g++) {
+        int64_t lo = group_offsets[g], hi = group_offsets[g + 1];
+        double sum = 0.0;
+        for (int64_t i = lo; i < hi; i++)
+            sum = sum + score[i];
+        group_score_out[g] = (hi > lo) ? sum / (double)(hi - lo) : 0.0;
+    }
+    return ORC_OK;
+}
+
+/* Trajectory keep flags from group keep flags: every member shares its
+ * group's fate. */
+int oracle_group_expand(const int64_t *group_offsets, int64_t n_groups, int64_t n,
+                        const uint8_t *group_keep, uint8_t *keep_out)
+{
+    if (n < 0 || n_groups < 0 || !group_offsets || (n_groups > 0 && !group_keep) ||
+        (n > 0 && !keep_out))
+        return ORC_ERR_ARG;
+    int rc = check_groups(group_offsets, n_groups, n);
+    if (rc != ORC_OK)
+        return rc;
+    for (int64_t g = 0; g < n_groups; g++)
+        for (int64_t i = group_offsets[g]; i < group_offsets[g + 1]; i++)
+            keep_out[i] = group_keep[g] ? 1 : 0;
+    return ORC_OK;
+}

@@ -45,9 +45,22 @@ MUTATIONS = [
     ("compact copies from packed position", "(const char *)cols_in[c] + (size_t)offsets[i] * e",
      "(const char *)cols_in[c] + (size_t)pos * e"),
     ("validate checks tag against V", "if (v < 0 || v > c)", "if (v < 0 || v > V)"),
+    ("group mean divides by size + 1", "sum / (double)(hi - lo) : 0.0", "sum / (double)(hi - lo + 1) : 0.0"),
+    ("group sum skips first member", "for (int64_t i = lo; i < hi; i++)\n            sum = sum + score[i];",
+     "for (int64_t i = lo + 1; i < hi; i++)\n            sum = sum + score[i];"),
+    ("group sum reads one past", "sum = sum + score[i];", "sum = sum + score[i < hi - 1 ? i + 1 : i];"),
+    ("empty group scores nonzero", ": 0.0;\n    }\n    return ORC_OK;", ": 1.0;\n    }\n    return ORC_OK;"),
+    ("group expand inverted", "keep_out[i] = group_keep[g] ? 1 : 0;", "keep_out[i] = group_keep[g] ? 0 : 1;"),
+    ("group expand off by one group", "keep_out[i] = group_keep[g] ? 1 : 0;",
+     "keep_out[i] = group_keep[g + 1 < n_groups ? g + 1 : g] ? 1 : 0;"),
+    ("group offsets end unchecked", "if (group_offsets[0] != 0 || group_offsets[n_groups] != n)",
+     "if (group_offsets[0] != 0)"),
 ]
 
-PIN_FUNCS = [getattr(pins, n) for n in dir(pins) if n.startswith("test_") and callable(getattr(pins, n))]
+from tests import test_oracle_group_pins as group_pins
+
+PIN_FUNCS = [getattr(m, n) for m in (pins, group_pins) for n in dir(m)
+             if n.startswith("test_") and callable(getattr(m, n))]
 
 
 def _run_pins():
@@ -55,7 +68,7 @@ def _run_pins():
     for f in PIN_FUNCS:
         try:
             f()
-        except Exception as e:   # assertion, oracle error, or hypothesis failure
+        except (Exception, pytest.fail.Exception) as e:   # assertion, oracle error, hypothesis, pytest.raises
             failed.append((f.__name__, type(e).__name__))
     return failed
 
