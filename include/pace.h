@@ -61,6 +61,7 @@ extern "C" {
 #define PACE_BAD_COMPLETION 0x2 /* some c_i < 0 or c_i > current_version */
 #define PACE_BAD_TAG 0x4        /* some tag < -1, or tag > c_i of its trajectory */
 #define PACE_BAD_WINDOW 0x8     /* prefix window not ascending, or holds NaN */
+#define PACE_BAD_GROUPS 0x10    /* group offsets not 0 .. n_traj non-decreasing (pace_validate_groups) */
 
 /* Controller parameters (host struct).
  *   w_wait     w_1 of Eq. (6): 1 for Effective and Raw Staleness, 0 for the
@@ -205,6 +206,58 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
                      const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
                      int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
                      size_t workspace_bytes, void *stream);
+
+/* ---- Group-level admission (Appendix B) ------------------------------------
+ * The full method aggregates by the mean within prompt groups; its score
+ * window and diagnostics count groups. Consecutive trajectories form prompt
+ * groups: group g holds trajectories [group_offsets[g], group_offsets[g+1]).
+ * group_offsets: int64 [n_groups + 1] device array, expected to start at 0,
+ * never decrease and end at n_traj (pace_validate_groups checks this; the
+ * other calls clamp every group offset to [0, n_traj], so malformed offsets
+ * give unspecified results but no out-of-bounds access). */
+
+/* pace_group_score -- the score of each group: the mean of its members'
+ * scores, added in member order and divided once by the member count. An
+ * empty group scores 0.
+ * score: f64 [n_traj] (pace_score output); group_score_out: f64 [n_groups]. */
+int pace_group_score(const double *score, int64_t n_traj, const int64_t *group_offsets, int64_t n_groups,
+                     double *group_score_out, void *stream);
+
+/* pace_group_expand -- trajectory keep flags from group keep flags: every
+ * member of group g gets (group_keep[g] != 0). keep_out: u8 [n_traj]; with
+ * well-formed group offsets every entry is written. */
+int pace_group_expand(const int64_t *group_offsets, int64_t n_groups, int64_t n_traj,
+                      const uint8_t *group_keep, uint8_t *keep_out, void *stream);
+
+/* pace_validate_groups -- writes PACE_BAD_GROUPS to *err_word_out (int32
+ * device scalar) when the group offsets are malformed, else 0. */
+int pace_validate_groups(const int64_t *group_offsets, int64_t n_groups, int64_t n_traj,
+                         int32_t *err_word_out, void *stream);
+
+/* pace_group_filter_step -- one filter step with prompt groups as the
+ * admission unit: pace_score, pace_group_score, pace_budget over groups
+ * (occupancy and capacity count groups), pace_select over the group scores
+ * (exactly *budget_out groups rejected, first in the order (group score desc,
+ * group id asc)), pace_group_expand and pace_compact, with the results of
+ * those calls made in sequence.
+ * group_score_out: f64 [n_groups]; group_keep_out: u8 [n_groups];
+ * reject_group_ids_out: int32, at least *budget_out entries (n_groups always
+ * suffice), ascending; keep_out: u8 [n_traj] (the expanded flags).
+ * Other arguments as pace_filter_step. workspace:
+ * pace_workspace_bytes(PACE_WS_FILTER_STEP, max(n_traj, n_groups), n_tokens)
+ * bytes. Argument errors (including a budget above n_groups) return before
+ * anything is enqueued, with *r_hat_inout unchanged. */
+int pace_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                           const int32_t *completion, int32_t current_version,
+                           const double *prefix_score, const double *window_sorted, int64_t window_n,
+                           const int64_t *group_offsets, int64_t n_groups, int64_t occupancy,
+                           int64_t capacity, const pace_params *params, double *r_hat_inout,
+                           int64_t *budget_out, double *score_out, int64_t *gen_sum_out,
+                           int64_t *gen_count_out, double *group_score_out, uint8_t *group_keep_out,
+                           int32_t *reject_group_ids_out, uint8_t *keep_out, int n_cols,
+                           const void *const *cols_in, const int32_t *elem_bytes, void *const *cols_out,
+                           int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
+                           void *workspace, size_t workspace_bytes, void *stream);
 
 /* pace_time_next_kernel -- measurement hook, not part of the method.
  * Arms a one-shot timer for one phase of the device work on the calling host

@@ -30,7 +30,7 @@ __all__ = [
 ]
 
 WS_SCORE, WS_SELECT, WS_COMPACT, WS_FILTER_STEP = 0, 1, 2, 3
-BAD_OFFSETS, BAD_COMPLETION, BAD_TAG, BAD_WINDOW = 0x1, 0x2, 0x4, 0x8
+BAD_OFFSETS, BAD_COMPLETION, BAD_TAG, BAD_WINDOW, BAD_GROUPS = 0x1, 0x2, 0x4, 0x8, 0x10
 PHASE_REDUCE, PHASE_FINALIZE, PHASE_SELECT, PHASE_COMPACT = 0, 1, 2, 3
 
 
@@ -253,6 +253,94 @@ def pace_filter_step(tags, offsets, completion, current_version, occupancy, capa
                                   _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_filter_step")
     return dict(budget=int(b.value), r_hat=float(rh.value), score=score_out, gen_sum=gen_sum_out,
                 gen_count=gen_count_out, keep=keep_out, reject_ids=reject_ids_out[: int(b.value)],
+                offsets_out=offsets_out, kept_ids=kept_ids_out, n_kept_tokens=n_kept_tokens_out,
+                cols_out=cols_out)
+
+
+def pace_group_score(score, group_offsets, group_score_out=None, stream=None):
+    """Mean member score of each prompt group (empty group: 0)."""
+    _dev(score, torch.float64, "score")
+    _dev(group_offsets, torch.int64, "group_offsets")
+    ng = group_offsets.numel() - 1
+    if group_score_out is None:
+        group_score_out = torch.empty(ng, dtype=torch.float64, device=score.device)
+    _check(lib().pace_group_score(_ptr(score), score.numel(), _ptr(group_offsets), ng, _ptr(group_score_out),
+                                  _stream(score.device, stream)), "pace_group_score")
+    return group_score_out
+
+
+def pace_group_expand(group_offsets, group_keep, n_traj: int, keep_out=None, stream=None):
+    """Trajectory keep flags from group keep flags."""
+    _dev(group_offsets, torch.int64, "group_offsets")
+    _dev(group_keep, torch.uint8, "group_keep")
+    ng = group_offsets.numel() - 1
+    if keep_out is None:
+        keep_out = torch.empty(int(n_traj), dtype=torch.uint8, device=group_keep.device)
+    _check(lib().pace_group_expand(_ptr(group_offsets), ng, int(n_traj), _ptr(group_keep), _ptr(keep_out),
+                                   _stream(group_keep.device, stream)), "pace_group_expand")
+    return keep_out
+
+
+def pace_validate_groups(group_offsets, n_traj: int, err_out=None, stream=None):
+    """Device check of the group offsets; returns the int32 error word tensor."""
+    _dev(group_offsets, torch.int64, "group_offsets")
+    dev = group_offsets.device
+    if err_out is None:
+        err_out = torch.empty(1, dtype=torch.int32, device=dev)
+    _check(lib().pace_validate_groups(_ptr(group_offsets), group_offsets.numel() - 1, int(n_traj),
+                                      _ptr(err_out), _stream(dev, stream)), "pace_validate_groups")
+    return err_out
+
+
+def pace_group_filter_step(tags, offsets, completion, current_version, group_offsets, occupancy, capacity,
+                           cols, prefix_score=None, window_sorted=None, params: Optional[PaceParams] = None,
+                           r_hat_prev: float = 0.0, workspace=None, stream=None):
+    """One filter step with prompt groups as the admission unit (occupancy and
+    capacity count groups). Returns a dict like pace_filter_step plus
+    group_score, group_keep and reject_group_ids (cut to the budget)."""
+    _dev(tags, torch.int32, "tags")
+    _dev(offsets, torch.int64, "offsets")
+    _dev(completion, torch.int32, "completion")
+    _dev(group_offsets, torch.int64, "group_offsets")
+    n = offsets.numel() - 1
+    ng = group_offsets.numel() - 1
+    nt = tags.numel()
+    dev = tags.device
+    W = 0
+    if prefix_score is not None:
+        _dev(prefix_score, torch.float64, "prefix_score")
+    if window_sorted is not None:
+        _dev(window_sorted, torch.float64, "window_sorted")
+        W = window_sorted.numel()
+    cols = list(cols)
+    for k, c in enumerate(cols):
+        if not c.is_cuda or not c.is_contiguous() or c.numel() != nt:
+            raise ValueError("column %d must be a contiguous device tensor of n_tokens elements" % k)
+    e = lambda k, dt: torch.empty(k, dtype=dt, device=dev)
+    score_out, gen_sum_out, gen_count_out = e(n, torch.float64), e(n, torch.int64), e(n, torch.int64)
+    group_score_out, group_keep_out = e(max(ng, 1), torch.float64), e(max(ng, 1), torch.uint8)
+    reject_group_ids_out = e(max(ng, 1), torch.int32)
+    keep_out = e(max(n, 1), torch.uint8)
+    cols_out = [torch.empty_like(c) for c in cols]
+    offsets_out, kept_ids_out = e(n + 1, torch.int64), e(max(n, 1), torch.int32)
+    n_kept_tokens_out = e(1, torch.int64)
+    ws = _workspace(WS_FILTER_STEP, max(n, ng), nt, dev, workspace)
+    nc = len(cols)
+    cin = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols])
+    cout = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols_out])
+    eb = (ctypes.c_int32 * max(nc, 1))(*[c.element_size() for c in cols])
+    rh = ctypes.c_double(float(r_hat_prev))
+    b = ctypes.c_int64(0)
+    _check(lib().pace_group_filter_step(
+        _ptr(tags), _ptr(offsets), n, nt, _ptr(completion), int(current_version), _ptr(prefix_score),
+        _ptr(window_sorted), W, _ptr(group_offsets), ng, int(occupancy), int(capacity),
+        ctypes.byref(params) if params is not None else None, ctypes.byref(rh), ctypes.byref(b),
+        _ptr(score_out), _ptr(gen_sum_out), _ptr(gen_count_out), _ptr(group_score_out), _ptr(group_keep_out),
+        _ptr(reject_group_ids_out), _ptr(keep_out), nc, cin, eb, cout, _ptr(offsets_out), _ptr(kept_ids_out),
+        _ptr(n_kept_tokens_out), _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_group_filter_step")
+    return dict(budget=int(b.value), r_hat=float(rh.value), score=score_out, gen_sum=gen_sum_out,
+                gen_count=gen_count_out, group_score=group_score_out[:ng], group_keep=group_keep_out[:ng],
+                reject_group_ids=reject_group_ids_out[: int(b.value)], keep=keep_out[:n],
                 offsets_out=offsets_out, kept_ids=kept_ids_out, n_kept_tokens=n_kept_tokens_out,
                 cols_out=cols_out)
 

@@ -161,6 +161,24 @@ hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64
                               int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, bool vec_ok,
                               hipStream_t stream);
 
+// ---- group-level admission ---------------------------------------------------
+hipError_t launch_group_score(const double *score, int64_t n, const int64_t *group_offsets, int64_t ng,
+                              double *group_score, hipStream_t stream);
+hipError_t launch_group_expand(const int64_t *group_offsets, int64_t ng, int64_t n, const uint8_t *group_keep,
+                               uint8_t *keep, hipStream_t stream);
+hipError_t launch_group_validate(const int64_t *group_offsets, int64_t ng, int64_t n, int32_t *err,
+                                 hipStream_t stream);
+// pace_group_filter_step's device work; ws is a filter-step workspace.
+hipError_t launch_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                                    const int32_t *completion, int32_t V, const double *prefix,
+                                    const double *window, int64_t W, bool use_prefix, double w_wait,
+                                    int gamma, const int64_t *group_offsets, int64_t ng, int64_t budget,
+                                    double *score, int64_t *gen_sum, int64_t *gen_count,
+                                    double *group_score, uint8_t *group_keep, int32_t *reject_group_ids,
+                                    uint8_t *keep, const CompactCols &cols, int n_cols,
+                                    int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
+                                    void *ws, bool vec_ok, hipStream_t stream);
+
 // ---- validate --------------------------------------------------------------
 hipError_t launch_validate(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                            const int32_t *completion, int32_t V, const double *window, int64_t W,

@@ -275,6 +275,86 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
     return PACE_OK;
 }
 
+static int check_groups_arg(const int64_t *group_offsets, int64_t n_groups) {
+    if (n_groups < 0 || n_groups >= INT32_MAX || !group_offsets || !aligned(group_offsets, 8))
+        return PACE_ERR_INVALID_ARG;
+    return PACE_OK;
+}
+
+int pace_group_score(const double *score, int64_t n_traj, const int64_t *group_offsets, int64_t n_groups,
+                     double *group_score_out, void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || check_groups_arg(group_offsets, n_groups) != PACE_OK)
+        return PACE_ERR_INVALID_ARG;
+    if ((n_traj > 0 && !score) || (n_groups > 0 && !group_score_out) || !aligned(score, 8) ||
+        !aligned(group_score_out, 8))
+        return PACE_ERR_INVALID_ARG;
+    return hip_status(launch_group_score(score, n_traj, group_offsets, n_groups, group_score_out,
+                                         (hipStream_t)stream));
+}
+
+int pace_group_expand(const int64_t *group_offsets, int64_t n_groups, int64_t n_traj,
+                      const uint8_t *group_keep, uint8_t *keep_out, void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || check_groups_arg(group_offsets, n_groups) != PACE_OK)
+        return PACE_ERR_INVALID_ARG;
+    if ((n_groups > 0 && !group_keep) || (n_traj > 0 && !keep_out)) return PACE_ERR_INVALID_ARG;
+    return hip_status(launch_group_expand(group_offsets, n_groups, n_traj, group_keep, keep_out,
+                                          (hipStream_t)stream));
+}
+
+int pace_validate_groups(const int64_t *group_offsets, int64_t n_groups, int64_t n_traj,
+                         int32_t *err_word_out, void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || check_groups_arg(group_offsets, n_groups) != PACE_OK)
+        return PACE_ERR_INVALID_ARG;
+    if (!err_word_out || !aligned(err_word_out, 4)) return PACE_ERR_INVALID_ARG;
+    return hip_status(launch_group_validate(group_offsets, n_groups, n_traj, err_word_out,
+                                            (hipStream_t)stream));
+}
+
+int pace_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                           const int32_t *completion, int32_t current_version,
+                           const double *prefix_score, const double *window_sorted, int64_t window_n,
+                           const int64_t *group_offsets, int64_t n_groups, int64_t occupancy,
+                           int64_t capacity, const pace_params *params, double *r_hat_inout,
+                           int64_t *budget_out, double *score_out, int64_t *gen_sum_out,
+                           int64_t *gen_count_out, double *group_score_out, uint8_t *group_keep_out,
+                           int32_t *reject_group_ids_out, uint8_t *keep_out, int n_cols,
+                           const void *const *cols_in, const int32_t *elem_bytes, void *const *cols_out,
+                           int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
+                           void *workspace, size_t workspace_bytes, void *stream) {
+    const pace_params p = params_or_default(params);
+    int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
+                              prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
+                              gen_count_out);
+    if (rc != PACE_OK) return rc;
+    if (check_groups_arg(group_offsets, n_groups) != PACE_OK) return PACE_ERR_INVALID_ARG;
+    if (n_groups > 0 && (!group_score_out || !group_keep_out)) return PACE_ERR_INVALID_ARG;
+    if (!aligned(group_score_out, 8) || !aligned(reject_group_ids_out, 4)) return PACE_ERR_INVALID_ARG;
+    CompactCols cols;
+    rc = check_compact_args(offsets, n_traj, n_tokens, keep_out, n_cols, cols_in, elem_bytes,
+                            cols_out, offsets_out, kept_ids_out, n_kept_tokens_out, &cols);
+    if (rc != PACE_OK) return rc;
+    if (!r_hat_inout || !budget_out) return PACE_ERR_INVALID_ARG;
+    const int64_t N = n_traj > n_groups ? n_traj : n_groups;
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < filter_step_ws_bytes(N, n_tokens))
+        return PACE_ERR_WORKSPACE;
+    double r_hat = *r_hat_inout;
+    int64_t budget = 0;
+    rc = pace_budget(occupancy, capacity, &p, &r_hat, &budget);
+    if (rc != PACE_OK) return rc;
+    if (budget > n_groups || (budget > 0 && !reject_group_ids_out)) return PACE_ERR_INVALID_ARG;
+    const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
+    const bool use_prefix = prefix_score != nullptr && window_n >= wmin;
+    rc = hip_status(launch_group_filter_step(
+        tags, offsets, n_traj, n_tokens, completion, current_version, prefix_score, window_sorted, window_n,
+        use_prefix, p.w_wait, p.gamma, group_offsets, n_groups, budget, score_out, gen_sum_out, gen_count_out,
+        group_score_out, group_keep_out, reject_group_ids_out, keep_out, cols, n_cols, offsets_out, kept_ids_out,
+        n_kept_tokens_out, workspace, aligned(tags, 16), (hipStream_t)stream));
+    if (rc != PACE_OK) return rc;
+    *r_hat_inout = r_hat;
+    *budget_out = budget;
+    return PACE_OK;
+}
+
 static_assert(PACE_PHASE_COUNT == kPhaseCount, "phase count");
 
 int pace_time_next_kernel(int phase, void *start_event, void *stop_event) {

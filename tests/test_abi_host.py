@@ -176,3 +176,34 @@ def test_time_next_kernel_arguments(L):
     assert L.pace_time_next_kernel(3, FAKE, FAKE) == 0
     for phase in range(4):
         assert L.pace_time_next_kernel(phase, None, None) == 0
+
+
+def test_group_host_argument_errors(L):
+    assert L.pace_group_score(FAKE, 10, None, 3, FAKE, None) == -1
+    assert L.pace_group_score(FAKE, 10, FAKE, -1, FAKE, None) == -1
+    assert L.pace_group_score(FAKE, 10, FAKE + 4, 3, FAKE, None) == -1       # misaligned offsets
+    assert L.pace_group_score(None, 10, FAKE, 3, FAKE, None) == -1
+    assert L.pace_group_expand(FAKE, 3, 10, None, FAKE, None) == -1
+    assert L.pace_group_expand(FAKE, 3, 10, FAKE, None, None) == -1
+    assert L.pace_validate_groups(FAKE, 3, 10, None, None) == -1
+    assert L.pace_validate_groups(FAKE, 3, -1, FAKE, None) == -1
+    import paper_2609_36830_amd as pace
+    p = pace.default_params()
+    rh = ctypes.c_double(0.5)
+    b = ctypes.c_int64(-3)
+    cols = (ctypes.c_void_p * 1)(FAKE)
+    e4 = (ctypes.c_int32 * 1)(4)
+
+    def call(go=FAKE, ng=4, occ=6, cap=4, gscore=FAKE, ws=FAKE, wsb=1 << 30, grej=FAKE):
+        return L.pace_group_filter_step(FAKE, FAKE, 20, 100, FAKE, 10, None, None, 0, go, ng, occ, cap,
+                                        ctypes.byref(p), ctypes.byref(rh), ctypes.byref(b), FAKE, None, None,
+                                        gscore, FAKE, grej, FAKE, 1, cols, e4, cols, FAKE, FAKE, FAKE, ws, wsb,
+                                        None)
+
+    assert call(go=None) == -1
+    assert call(gscore=None) == -1
+    assert call(occ=100, cap=0) == -1          # budget 90 > 4 groups
+    assert call(grej=None) == -1               # budget 4 > 0 needs reject ids
+    assert call(ws=None) == -2
+    assert call(wsb=64) == -2
+    assert rh.value == 0.5 and b.value == -3
