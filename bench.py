@@ -208,6 +208,27 @@ def main():
     kernel_us = {name: np.array([kev[k][ph][0].elapsed_time(kev[k][ph][1]) * 1e3 for k in range(K)])
                  for ph, name in enumerate(PHASES)}
 
+    # Group-level admission on the same pool: prompt groups of 8 trajectories,
+    # occupancy and target counted in groups (NEXT-1 row), cold steps.
+    go = torch.arange(0, pool.n + 1, 8, dtype=torch.int64, device=dev)
+    if int(go[-1]) != pool.n:
+        go = torch.cat([go, torch.tensor([pool.n], dtype=torch.int64, device=dev)])
+    n_groups = go.numel() - 1
+    g_occ, g_cap = n_groups, -(-pool.capacity // 8)
+    gws = torch.empty(pace.pace_workspace_bytes(pace.WS_FILTER_STEP, max(pool.n, n_groups), pool.n_tokens),
+                      dtype=torch.uint8, device=dev)
+    gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K + 2)]
+    g_res = None
+    for k in range(K + 2):
+        flush.max()
+        gev[k][0].record(stream)
+        g_res = pace.pace_group_filter_step(tags, off, comp, pool.V, go, g_occ, g_cap, cols, prefix, window,
+                                            params, 0.0, workspace=gws)
+        gev[k][1].record(stream)
+    torch.cuda.synchronize()
+    g_ms = np.array([e[0].elapsed_time(e[1]) for e in gev[2:]])
+    g_kept_tok = int(g_res["n_kept_tokens"].item())
+
     # Warm back-to-back steps (no flush) for context.
     warm_ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     torch.cuda.synchronize()
@@ -264,6 +285,15 @@ def main():
         "kernel_us_mean": {k: float(v.mean()) for k, v in kernel_us.items()},
         "kernel_us_p50": {k: float(np.median(v)) for k, v in kernel_us.items()},
         "warm_ms_per_step": warm_ms,
+        "group_step": {
+            "entry": "pace_group_filter_step (groups of 8, group mean score)",
+            "n_groups": n_groups, "occupancy_groups": g_occ, "target_groups": g_cap,
+            "budget_groups": g_res["budget"], "kept_tokens": g_kept_tok,
+            "ms_per_step": float(g_ms.mean()),
+            "tokens_per_s": pool.n_tokens / (float(g_ms.mean()) * 1e-3),
+            "hbm_frac_of_peak": (alg_bytes(pool, g_kept_tok, [c.element_size() for c in cols], W)[0]
+                                 + n_groups * (8 + 8 + 8 + 1 + 4) + pool.n) / (float(g_ms.mean()) * 1e-3) / HBM_PEAK,
+        },
         "wall_s_timed_region": wall,
         "roofline": {
             "kernel": "score_reduce",
