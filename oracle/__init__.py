@@ -53,8 +53,9 @@ def load_library(path: str):
     lib.oracle_compact.argtypes = [P, i64, i64, P, ctypes.c_int, P, P, P, P, P, P]
     lib.oracle_group_score.argtypes = [P, i64, P, i64, P]
     lib.oracle_group_expand.argtypes = [P, i64, i64, P, P]
+    lib.oracle_stream_admit.argtypes = [P, i64, d, d, i64, i64, P, i64, P, P, P, P, P, P]
     for f in ("oracle_validate", "oracle_score", "oracle_budget", "oracle_select", "oracle_compact",
-              "oracle_group_score", "oracle_group_expand"):
+              "oracle_group_score", "oracle_group_expand", "oracle_stream_admit"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -228,4 +229,43 @@ def group_filter_step(pool, group_offsets, occupancy, capacity, mode="effective"
     return dict(score=sc, S=S, T=T, group_score=gs, budget=b, r_hat=r_hat, group_keep=gkeep,
                 reject_group_ids=grej, keep=keep, offsets_out=off_out, kept_ids=ids, packed=packed,
                 n_kept_tokens=int(off_out[-1]))
+
+
+class StreamWindow:
+    """The sliding window of observed scores (a ring of `cap` entries)."""
+
+    def __init__(self, cap=512):
+        self.ring = np.zeros(cap, np.float64)
+        self.cap, self.head, self.count = cap, 0, 0
+
+    def copy(self):
+        w = StreamWindow(self.cap)
+        w.ring[:] = self.ring
+        w.head, w.count = self.head, self.count
+        return w
+
+    def entries(self):
+        """The window's scores, oldest first."""
+        return np.array([self.ring[(self.head - self.count + t) % self.cap] for t in range(self.count)])
+
+
+def stream_admit(score_arr, r_hat, window: StreamWindow, batch_size, r_max=0.9, window_min=32, check=True):
+    """One step of the streaming rule; updates `window` in place. Returns
+    (status uint8[n]: 0 rejected, 1 retained, 2 not drawn; kappa; n_drawn; n_retained)."""
+    s = _c(score_arr, np.float64)
+    n = s.shape[0]
+    status = np.empty(max(n, 1), np.uint8)
+    head, cnt = ctypes.c_int64(window.head), ctypes.c_int64(window.count)
+    kappa = ctypes.c_double(0.0)
+    drawn, kept = ctypes.c_int64(0), ctypes.c_int64(0)
+    rc = _load().oracle_stream_admit(_p(s), n, float(r_hat), float(r_max), int(window_min), int(batch_size),
+                                     _p(window.ring), window.cap, ctypes.addressof(head), ctypes.addressof(cnt),
+                                     _p(status), ctypes.addressof(kappa), ctypes.addressof(drawn),
+                                     ctypes.addressof(kept))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_stream_admit")
+        return rc
+    window.head, window.count = int(head.value), int(cnt.value)
+    return status[:n].copy(), float(kappa.value), int(drawn.value), int(kept.value)
 

@@ -324,3 +324,92 @@ int oracle_group_expand(const int64_t *group_offsets, int64_t n_groups, int64_t 
             keep_out[i] = group_keep[g] ? 1 : 0;
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------
+ * The streaming admission rule (Sec. 3.1, Algorithm 1), literally: at step j
+ * the cutoff kappa is the (1 - r_hat)-quantile of a sliding window of
+ * recently observed scores; the trainer then draws candidates from the pool
+ * in pool order, observes each one's score, rejects it when its score exceeds
+ * kappa and retains it otherwise, until batch_size candidates are retained
+ * or the pool is exhausted.
+ *
+ * Readings (the paper leaves these open):
+ *   - kappa is fixed for the whole step, from the window as it stood before
+ *     the draw; every drawn candidate's score then enters the window, in draw
+ *     order, after the draw;
+ *   - the quantile is the lower empirical one: the ceil(p * cnt)-th smallest
+ *     of the cnt window entries, p = 1 - min(r_hat, r_max);
+ *   - with fewer than window_min entries, or a rate of 0, nothing is
+ *     rejected (kappa = +inf);
+ *   - the window is a ring of window_cap entries: once full, each new score
+ *     replaces the oldest.
+ * status_out[i]: 0 drawn and rejected, 1 drawn and retained, 2 not drawn.
+ * ---------------------------------------------------------------------- */
+static int cmp_double_asc(const void *pa, const void *pb)
+{
+    double x = *(const double *)pa, y = *(const double *)pb;
+    if (x < y)
+        return -1;
+    return x > y ? 1 : 0;
+}
+
+int oracle_stream_admit(const double *score, int64_t n, double r_hat, double r_max,
+                        int64_t window_min, int64_t batch_size, double *ring, int64_t cap,
+                        int64_t *head_inout, int64_t *count_inout, uint8_t *status_out,
+                        double *kappa_out, int64_t *n_drawn_out, int64_t *n_retained_out)
+{
+    if (n < 0 || cap < 1 || batch_size < 0 || window_min < 0 || !ring || !head_inout ||
+        !count_inout || !kappa_out || !n_drawn_out || !n_retained_out ||
+        (n > 0 && (!score || !status_out)))
+        return ORC_ERR_ARG;
+    int64_t head = *head_inout, cnt = *count_inout;
+    if (head < 0 || head >= cap || cnt < 0 || cnt > cap || !(r_hat >= 0.0) || !(r_max >= 0.0))
+        return ORC_ERR_ARG;
+
+    /* the cutoff, from the window before this step's draw */
+    double rate = r_hat < r_max ? r_hat : r_max;
+    double kappa = INFINITY;
+    if (cnt >= window_min && cnt > 0 && rate > 0.0) {
+        double *sorted = (double *)malloc((size_t)cnt * sizeof(double));
+        if (!sorted)
+            return ORC_ERR_ARG;
+        /* the cnt most recent entries end just before head */
+        for (int64_t t = 0; t < cnt; t++)
+            sorted[t] = ring[(head - cnt + t + cap) % cap];
+        qsort(sorted, (size_t)cnt, sizeof(double), cmp_double_asc);
+        double p = 1.0 - rate;
+        int64_t k = (int64_t)ceil(p * (double)cnt);   /* 1-based rank */
+        if (k < 1)
+            k = 1;
+        kappa = sorted[k - 1];
+        free(sorted);
+    }
+
+    /* the draw */
+    int64_t drawn = 0, retained = 0;
+    for (int64_t i = 0; i < n; i++)
+        status_out[i] = 2;
+    for (int64_t i = 0; i < n && retained < batch_size; i++) {
+        drawn += 1;
+        if (score[i] > kappa) {
+            status_out[i] = 0;
+        } else {
+            status_out[i] = 1;
+            retained += 1;
+        }
+    }
+
+    /* the window takes every drawn score, oldest first */
+    for (int64_t i = 0; i < drawn; i++) {
+        ring[head] = score[i];
+        head = (head + 1) % cap;
+        if (cnt < cap)
+            cnt += 1;
+    }
+    *head_inout = head;
+    *count_inout = cnt;
+    *kappa_out = kappa;
+    *n_drawn_out = drawn;
+    *n_retained_out = retained;
+    return ORC_OK;
+}

@@ -55,11 +55,25 @@ MUTATIONS = [
      "keep_out[i] = group_keep[g + 1 < n_groups ? g + 1 : g] ? 1 : 0;"),
     ("group offsets end unchecked", "if (group_offsets[0] != 0 || group_offsets[n_groups] != n)",
      "if (group_offsets[0] != 0)"),
+    ("stream quantile rank rounds down", "int64_t k = (int64_t)ceil(p * (double)cnt);",
+     "int64_t k = (int64_t)floor(p * (double)cnt);"),
+    ("stream quantile of the rate, not its complement", "double p = 1.0 - rate;", "double p = rate;"),
+    ("stream rate not capped", "double rate = r_hat < r_max ? r_hat : r_max;", "double rate = r_hat;"),
+    ("stream rejects ties with the cutoff", "if (score[i] > kappa) {", "if (score[i] >= kappa) {"),
+    ("stream window ignores min observations", "if (cnt >= window_min && cnt > 0 && rate > 0.0) {",
+     "if (cnt > 0 && rate > 0.0) {"),
+    ("stream draw runs one past the batch", "for (int64_t i = 0; i < n && retained < batch_size; i++) {",
+     "for (int64_t i = 0; i < n && retained <= batch_size; i++) {"),
+    ("stream window takes only retained scores", "        ring[head] = score[i];\n        head = (head + 1) % cap;",
+     "        if (status_out[i] != 1) continue;\n        ring[head] = score[i];\n        head = (head + 1) % cap;"),
+    ("stream window misses the newest entry", "sorted[t] = ring[(head - cnt + t + cap) % cap];",
+     "sorted[t] = ring[(head - cnt + t + cap - 1) % cap];"),
 ]
 
 from tests import test_oracle_group_pins as group_pins
+from tests import test_oracle_stream_pins as stream_pins
 
-PIN_FUNCS = [getattr(m, n) for m in (pins, group_pins) for n in dir(m)
+PIN_FUNCS = [getattr(m, n) for m in (pins, group_pins, stream_pins) for n in dir(m)
              if n.startswith("test_") and callable(getattr(m, n))]
 
 
