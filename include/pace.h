@@ -259,6 +259,39 @@ int pace_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t 
                            int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
                            void *workspace, size_t workspace_bytes, void *stream);
 
+/* ---- The streaming admission rule (Sec. 3.1, Algorithm 1) ------------------
+ * pace_stream_admit -- one step of the paper's rule as written: the cutoff
+ * kappa is the (1 - rate)-quantile of a sliding window of recently observed
+ * scores, rate = min(r_hat, params->r_max); candidates are drawn in pool order,
+ * a candidate scoring above kappa is rejected, the others are retained, until
+ * batch_size are retained or the pool is exhausted. The realised number of
+ * rejections varies (pace_select instead rejects exactly a budget).
+ * Readings: kappa is fixed for the step from the window as it stood before
+ * the draw, and is the lower empirical quantile, the ceil(p * cnt)-th
+ * smallest of the cnt window entries with p = 1 - rate evaluated in binary64;
+ * with fewer than params->window_min entries, or rate 0, nothing is rejected
+ * (kappa = +inf); every drawn candidate's score then enters the window, in
+ * draw order, the oldest entries giving way once the window is full.
+ *
+ * score: f64 [n_traj] (pace_score output; must not hold NaN).
+ * r_hat: [host] smoothed rejection rate (pace_budget's r_hat).
+ * batch_size: candidates to retain (>= 0).
+ * window_ring: f64 [window_cap] device ring of observed scores, and
+ * window_state: int64 [2] device {head, count}: the next slot to write and the
+ *   number of valid entries (the count entries before head, cyclically).
+ *   A fresh window is {0, 0}. Both are updated in place. 1 <= window_cap <= 1024.
+ * status_out: u8 [n_traj]: 0 drawn and rejected, 1 drawn and retained,
+ *   2 not drawn (stays in the pool). keep_out: u8 [n_traj], 1 = retained
+ *   (pass it to pace_compact to build the batch).
+ * reject_ids_out: int32, the rejected ids ascending (n_traj entries suffice).
+ * kappa_out: f64 device scalar. counts_out: int64 [3] device: drawn,
+ *   retained, rejected.
+ * One workgroup; no workspace. */
+int pace_stream_admit(const double *score, int64_t n_traj, double r_hat, const pace_params *params,
+                      int64_t batch_size, double *window_ring, int64_t window_cap, int64_t *window_state,
+                      uint8_t *status_out, uint8_t *keep_out, int32_t *reject_ids_out, double *kappa_out,
+                      int64_t *counts_out, void *stream);
+
 /* pace_time_next_kernel -- measurement hook, not part of the method.
  * Arms a one-shot timer for one phase of the device work on the calling host
  * thread: the next kernel of that phase launched from this thread (by any

@@ -345,6 +345,37 @@ def pace_group_filter_step(tags, offsets, completion, current_version, group_off
                 cols_out=cols_out)
 
 
+class StreamWindow:
+    """Device state of the streaming rule's score window: a ring of `cap`
+    scores and its {head, count} pair (a fresh window is empty)."""
+
+    def __init__(self, cap=512, device="cuda"):
+        self.ring = torch.zeros(cap, dtype=torch.float64, device=device)
+        self.state = torch.zeros(2, dtype=torch.int64, device=device)
+        self.cap = cap
+
+
+def pace_stream_admit(score, r_hat: float, window: StreamWindow, batch_size: int,
+                      params: Optional[PaceParams] = None, status_out=None, keep_out=None,
+                      reject_ids_out=None, kappa_out=None, counts_out=None, stream=None):
+    """One step of the streaming rule. Returns (status, keep, reject_ids, kappa,
+    counts) as device tensors; counts = [drawn, retained, rejected]."""
+    _dev(score, torch.float64, "score")
+    n = score.numel()
+    dev = score.device
+    e = lambda k, dt: torch.empty(k, dtype=dt, device=dev)
+    status_out = e(max(n, 1), torch.uint8) if status_out is None else status_out
+    keep_out = e(max(n, 1), torch.uint8) if keep_out is None else keep_out
+    reject_ids_out = e(max(n, 1), torch.int32) if reject_ids_out is None else reject_ids_out
+    kappa_out = e(1, torch.float64) if kappa_out is None else kappa_out
+    counts_out = e(3, torch.int64) if counts_out is None else counts_out
+    _check(lib().pace_stream_admit(_ptr(score), n, float(r_hat), ctypes.byref(params) if params is not None else None,
+                                   int(batch_size), _ptr(window.ring), window.cap, _ptr(window.state),
+                                   _ptr(status_out), _ptr(keep_out), _ptr(reject_ids_out), _ptr(kappa_out),
+                                   _ptr(counts_out), _stream(dev, stream)), "pace_stream_admit")
+    return status_out[:n], keep_out[:n], reject_ids_out, kappa_out, counts_out
+
+
 def pace_time_next_kernel(phase: int, start=None, stop=None):
     """Arm a one-shot timer on the next kernel of `phase` launched from this
     thread. start/stop are torch.cuda.Event(enable_timing=True) objects that

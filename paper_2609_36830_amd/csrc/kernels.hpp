@@ -179,6 +179,12 @@ hipError_t launch_group_filter_step(const int32_t *tags, const int64_t *offsets,
                                     int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
                                     void *ws, bool vec_ok, hipStream_t stream);
 
+// ---- streaming admission rule ------------------------------------------------
+constexpr int64_t kStreamWindowMax = 1024;   // largest score window (ring entries)
+hipError_t launch_stream_admit(const double *score, int64_t n, double rate, int64_t window_min, int64_t B,
+                               double *ring, int64_t cap, int64_t *state, uint8_t *status, uint8_t *keep,
+                               int32_t *reject_ids, double *kappa, int64_t *counts, hipStream_t stream);
+
 // ---- validate --------------------------------------------------------------
 hipError_t launch_validate(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                            const int32_t *completion, int32_t V, const double *window, int64_t W,

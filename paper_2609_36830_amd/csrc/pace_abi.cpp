@@ -355,6 +355,27 @@ int pace_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t 
     return PACE_OK;
 }
 
+int pace_stream_admit(const double *score, int64_t n_traj, double r_hat, const pace_params *params,
+                      int64_t batch_size, double *window_ring, int64_t window_cap, int64_t *window_state,
+                      uint8_t *status_out, uint8_t *keep_out, int32_t *reject_ids_out, double *kappa_out,
+                      int64_t *counts_out, void *stream) {
+    const pace_params p = params_or_default(params);
+    if (n_traj < 0 || n_traj >= INT32_MAX || batch_size < 0) return PACE_ERR_INVALID_ARG;
+    if (!(r_hat >= 0.0) || isinf(r_hat) || !(p.r_max >= 0.0 && p.r_max <= 1.0) || p.window_min < 0)
+        return PACE_ERR_INVALID_ARG;
+    if (window_cap < 1 || window_cap > kStreamWindowMax || !window_ring || !window_state || !kappa_out ||
+        !counts_out)
+        return PACE_ERR_INVALID_ARG;
+    if (n_traj > 0 && (!score || !status_out || !keep_out || !reject_ids_out)) return PACE_ERR_INVALID_ARG;
+    if (!aligned(score, 8) || !aligned(window_ring, 8) || !aligned(window_state, 8) || !aligned(kappa_out, 8) ||
+        !aligned(counts_out, 8) || !aligned(reject_ids_out, 4))
+        return PACE_ERR_INVALID_ARG;
+    const double rate = r_hat < p.r_max ? r_hat : p.r_max;
+    return hip_status(launch_stream_admit(score, n_traj, rate, p.window_min, batch_size, window_ring,
+                                          window_cap, window_state, status_out, keep_out, reject_ids_out,
+                                          kappa_out, counts_out, (hipStream_t)stream));
+}
+
 static_assert(PACE_PHASE_COUNT == kPhaseCount, "phase count");
 
 int pace_time_next_kernel(int phase, void *start_event, void *stop_event) {

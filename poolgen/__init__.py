@@ -278,3 +278,22 @@ def refresh_slots(pool: Pool, step: int, frac: float = 0.05, seed_base: int = 0)
         new_tags.append(np.repeat(vers.astype(np.int32), np.diff(bounds)))
         new_c[k] = c
     return slots, (np.concatenate(new_tags) if new_tags else np.empty(0, np.int32)), new_c
+
+
+def sweep_step(pool: Pool, step: int, V0: int, frac: float = 0.05, seed_base: int = 0):
+    """Advances a pool in place to step ``step`` of a back-to-back sweep: the
+    current version becomes V0 + step and ``frac`` of the slots are refreshed
+    as freshly completed, never-interrupted rollouts (refresh_slots; their
+    prefix score becomes NaN). Returns the refreshed slot ids, so that a
+    device copy can be updated span by span."""
+    pool.V = V0 + step
+    slots, new_tags, new_c = refresh_slots(pool, step, frac, seed_base)
+    pos = 0
+    for k, i in enumerate(slots):
+        lo, hi = int(pool.offsets[i]), int(pool.offsets[i + 1])
+        pool.tags[lo:hi] = new_tags[pos:pos + hi - lo]
+        pos += hi - lo
+        pool.completion[i] = new_c[k]
+        if pool.prefix_score is not None:
+            pool.prefix_score[i] = np.nan
+    return slots

@@ -207,3 +207,18 @@ def test_group_host_argument_errors(L):
     assert call(ws=None) == -2
     assert call(wsb=64) == -2
     assert rh.value == 0.5 and b.value == -3
+
+
+def test_stream_admit_host_argument_errors(L):
+    def call(n=10, r_hat=0.5, B=4, ring=FAKE, cap=512, state=FAKE, status=FAKE):
+        return L.pace_stream_admit(FAKE, n, r_hat, None, B, ring, cap, state, status, FAKE, FAKE, FAKE, FAKE, None)
+
+    assert call(cap=0) == -1
+    assert call(cap=1025) == -1
+    assert call(r_hat=float("nan")) == -1
+    assert call(r_hat=-0.1) == -1
+    assert call(B=-1) == -1
+    assert call(n=-1) == -1
+    assert call(ring=None) == -1
+    assert call(state=None) == -1
+    assert call(status=None) == -1
