@@ -40,6 +40,8 @@ def parse():
                     help="payload columns: 1 = tags; 3 = tags + token ids + fp32 log-probs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--sweep-steps", type=int, default=256,
+                    help="steps of the back-to-back streaming-rule sweep (0 = skip)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run one plain 256 MiB device copy (counter calibration)")
     return ap.parse_args()
@@ -80,6 +82,64 @@ REDUCE_COUNTERS = {
     # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98115.5 KiB, WRITE_SIZE 273.7 KiB
     "stress": {"sha256": "7784683db2f83137ed858820ca0f9134061992691cb1499722615668dfae9ce3", "bytes": 201220813},
 }
+
+
+def stream_sweep(args, pace, pool, tags, off, comp, prefix, window, cols, dev, stream):
+    """Back-to-back sweep with the streaming admission rule (no cache flush):
+    per step s the current version is V0 + s and 5% of the slots are refreshed
+    as fresh rollouts (host generation and upload outside the events); the
+    timed step is one pace_stream_step call: pace_budget (beta 0.9, r_hat
+    carried), pace_score, one pace_stream_admit draw of a batch of
+    ceil(target / 3) and pace_compact of the retained batch. Runs on copies of
+    the pool."""
+    import copy
+    import torch
+    import poolgen
+    spool = copy.deepcopy(pool)
+    V0 = spool.V
+    stags, scomp = tags.clone(), comp.clone()
+    spre = prefix.clone() if prefix is not None else None
+    scols = [stags] + list(cols[1:])
+    n, nt = pool.n, pool.n_tokens
+    params = pace.default_params(beta=0.9, w_wait=0.0 if args.mode == "gen" else 1.0)
+    batch = -(-pool.capacity // 3)
+    win = pace.StreamWindow(512, dev)
+    bufs = pace.stream_step_buffers(n, nt, [c.dtype for c in scols], dev)
+    counts = torch.empty(args.sweep_steps * 3, dtype=torch.int64, device=dev)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.sweep_steps)]
+    r_hat = 0.0
+    for step in range(args.sweep_steps):
+        slots = poolgen.sweep_step(spool, step, V0)
+        lo, hi = int(spool.offsets[slots.min()]), int(spool.offsets[slots.max() + 1])
+        if slots.max() - slots.min() + 1 == len(slots):
+            stags[lo:hi].copy_(torch.from_numpy(spool.tags[lo:hi]), non_blocking=False)
+        else:
+            stags.copy_(torch.from_numpy(spool.tags))
+        scomp.copy_(torch.from_numpy(spool.completion))
+        if spre is not None:
+            spre.copy_(torch.from_numpy(spool.prefix_score))
+        # keep the device busy (a short spin, no memory traffic) while the host
+        # issues the step, so the events time the step's kernels, not the
+        # host's call overhead
+        torch.cuda._sleep(400000)
+        evs[step][0].record(stream)
+        _, r_hat = pace.pace_stream_step(stags, off, scomp, spool.V, spool.occupancy, spool.capacity, scols,
+                                         win, batch, spre, window, params, r_hat, bufs)
+        evs[step][1].record(stream)
+        counts[3 * step: 3 * step + 3].copy_(bufs["counts"])
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in evs])
+    c = counts.view(-1, 3).cpu().numpy()
+    return {
+        "entry": "pace_stream_step (budget, score, stream admit, compact), back to back, no flush",
+        "steps": args.sweep_steps, "batch": batch, "beta": 0.9, "window": 512,
+        "ms_per_step": float(ms.mean()), "ms_p10_p50_p90": [float(np.percentile(ms, q)) for q in (10, 50, 90)],
+        "tokens_per_s": nt / (float(ms.mean()) * 1e-3),
+        "final_r_hat": r_hat,
+        "mean_drawn": float(c[:, 0].mean()), "mean_retained": float(c[:, 1].mean()),
+        "mean_rejected": float(c[:, 2].mean()), "last_rejected": int(c[-1, 2]),
+    }
 
 
 def alg_bytes(pool, n_keep_tok, col_bytes, W):
@@ -239,6 +299,9 @@ def main():
     torch.cuda.synchronize()
     warm_ms = warm_ev[0].elapsed_time(warm_ev[1]) / K
 
+    sweep = stream_sweep(args, pace, pool, tags, off, comp, prefix, window, cols, dev, stream) \
+        if args.sweep_steps > 0 else None
+
     if args.calib_copy:
         a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
         b = torch.empty_like(a)
@@ -285,6 +348,7 @@ def main():
         "kernel_us_mean": {k: float(v.mean()) for k, v in kernel_us.items()},
         "kernel_us_p50": {k: float(np.median(v)) for k, v in kernel_us.items()},
         "warm_ms_per_step": warm_ms,
+        "stream_sweep": sweep,
         "group_step": {
             "entry": "pace_group_filter_step (groups of 8, group mean score)",
             "n_groups": n_groups, "occupancy_groups": g_occ, "target_groups": g_cap,

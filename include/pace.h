@@ -292,6 +292,24 @@ int pace_stream_admit(const double *score, int64_t n_traj, double r_hat, const p
                       uint8_t *status_out, uint8_t *keep_out, int32_t *reject_ids_out, double *kappa_out,
                       int64_t *counts_out, void *stream);
 
+/* pace_stream_step -- one whole trainer step under the streaming rule:
+ * pace_budget on the host (r_hat carried in *r_hat_inout), then pace_score,
+ * pace_stream_admit and pace_compact of the retained batch on the device,
+ * with the results of those calls made in sequence. Arguments as in those
+ * calls; workspace: pace_workspace_bytes(PACE_WS_FILTER_STEP, n_traj,
+ * n_tokens) bytes. Argument errors return before anything is enqueued, with
+ * *r_hat_inout unchanged. */
+int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                     const int32_t *completion, int32_t current_version, const double *prefix_score,
+                     const double *window_sorted, int64_t window_n, int64_t occupancy, int64_t capacity,
+                     const pace_params *params, double *r_hat_inout, int64_t batch_size,
+                     double *window_ring, int64_t window_cap, int64_t *window_state, double *score_out,
+                     int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *status_out, uint8_t *keep_out,
+                     int32_t *reject_ids_out, double *kappa_out, int64_t *counts_out, int n_cols,
+                     const void *const *cols_in, const int32_t *elem_bytes, void *const *cols_out,
+                     int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
+                     void *workspace, size_t workspace_bytes, void *stream);
+
 /* pace_time_next_kernel -- measurement hook, not part of the method.
  * Arms a one-shot timer for one phase of the device work on the calling host
  * thread: the next kernel of that phase launched from this thread (by any

@@ -376,6 +376,53 @@ def pace_stream_admit(score, r_hat: float, window: StreamWindow, batch_size: int
     return status_out[:n], keep_out[:n], reject_ids_out, kappa_out, counts_out
 
 
+def stream_step_buffers(n: int, n_tokens: int, col_dtypes: Sequence[torch.dtype], device):
+    """Preallocated outputs for repeated pace_stream_step calls."""
+    e = lambda k, dt: torch.empty(k, dtype=dt, device=device)
+    return dict(score=e(max(n, 1), torch.float64), gen_sum=e(max(n, 1), torch.int64),
+                gen_count=e(max(n, 1), torch.int64), status=e(max(n, 1), torch.uint8),
+                keep=e(max(n, 1), torch.uint8), reject_ids=e(max(n, 1), torch.int32),
+                kappa=e(1, torch.float64), counts=e(3, torch.int64),
+                cols_out=[e(max(n_tokens, 1), dt) for dt in col_dtypes], offsets_out=e(n + 1, torch.int64),
+                kept_ids=e(max(n, 1), torch.int32), n_kept_tokens=e(1, torch.int64),
+                workspace=e(max(pace_workspace_bytes(WS_FILTER_STEP, n, n_tokens), 256), torch.uint8))
+
+
+def pace_stream_step(tags, offsets, completion, current_version, occupancy, capacity, cols,
+                     window: StreamWindow, batch_size: int, prefix_score=None, window_sorted=None,
+                     params: Optional[PaceParams] = None, r_hat_prev: float = 0.0, buffers=None, stream=None):
+    """One trainer step under the streaming rule (budget, score, draw, compact
+    of the retained batch). Returns (buffers dict, r_hat)."""
+    _dev(tags, torch.int32, "tags")
+    _dev(offsets, torch.int64, "offsets")
+    _dev(completion, torch.int32, "completion")
+    n = offsets.numel() - 1
+    nt = tags.numel()
+    dev = tags.device
+    W = 0
+    if prefix_score is not None:
+        _dev(prefix_score, torch.float64, "prefix_score")
+    if window_sorted is not None:
+        _dev(window_sorted, torch.float64, "window_sorted")
+        W = window_sorted.numel()
+    cols = list(cols)
+    b = buffers if buffers is not None else stream_step_buffers(n, nt, [c.dtype for c in cols], dev)
+    nc = len(cols)
+    cin = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols])
+    cout = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in b["cols_out"]])
+    eb = (ctypes.c_int32 * max(nc, 1))(*[c.element_size() for c in cols])
+    rh = ctypes.c_double(float(r_hat_prev))
+    ws = b["workspace"]
+    _check(lib().pace_stream_step(
+        _ptr(tags), _ptr(offsets), n, nt, _ptr(completion), int(current_version), _ptr(prefix_score),
+        _ptr(window_sorted), W, int(occupancy), int(capacity), ctypes.byref(params) if params is not None else None,
+        ctypes.byref(rh), int(batch_size), _ptr(window.ring), window.cap, _ptr(window.state), _ptr(b["score"]),
+        _ptr(b["gen_sum"]), _ptr(b["gen_count"]), _ptr(b["status"]), _ptr(b["keep"]), _ptr(b["reject_ids"]),
+        _ptr(b["kappa"]), _ptr(b["counts"]), nc, cin, eb, cout, _ptr(b["offsets_out"]), _ptr(b["kept_ids"]),
+        _ptr(b["n_kept_tokens"]), _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_stream_step")
+    return b, float(rh.value)
+
+
 def pace_time_next_kernel(phase: int, start=None, stop=None):
     """Arm a one-shot timer on the next kernel of `phase` launched from this
     thread. start/stop are torch.cuda.Event(enable_timing=True) objects that

@@ -376,6 +376,61 @@ int pace_stream_admit(const double *score, int64_t n_traj, double r_hat, const p
                                           kappa_out, counts_out, (hipStream_t)stream));
 }
 
+int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                     const int32_t *completion, int32_t current_version, const double *prefix_score,
+                     const double *window_sorted, int64_t window_n, int64_t occupancy, int64_t capacity,
+                     const pace_params *params, double *r_hat_inout, int64_t batch_size,
+                     double *window_ring, int64_t window_cap, int64_t *window_state, double *score_out,
+                     int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *status_out, uint8_t *keep_out,
+                     int32_t *reject_ids_out, double *kappa_out, int64_t *counts_out, int n_cols,
+                     const void *const *cols_in, const int32_t *elem_bytes, void *const *cols_out,
+                     int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
+                     void *workspace, size_t workspace_bytes, void *stream) {
+    const pace_params p = params_or_default(params);
+    int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
+                              prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
+                              gen_count_out);
+    if (rc != PACE_OK) return rc;
+    CompactCols cols;
+    rc = check_compact_args(offsets, n_traj, n_tokens, keep_out, n_cols, cols_in, elem_bytes,
+                            cols_out, offsets_out, kept_ids_out, n_kept_tokens_out, &cols);
+    if (rc != PACE_OK) return rc;
+    if (!r_hat_inout || batch_size < 0 || window_cap < 1 || window_cap > kStreamWindowMax || !window_ring ||
+        !window_state || !kappa_out || !counts_out)
+        return PACE_ERR_INVALID_ARG;
+    if (n_traj > 0 && (!status_out || !keep_out || !reject_ids_out)) return PACE_ERR_INVALID_ARG;
+    if (!aligned(window_ring, 8) || !aligned(window_state, 8) || !aligned(kappa_out, 8) ||
+        !aligned(counts_out, 8) || !aligned(reject_ids_out, 4))
+        return PACE_ERR_INVALID_ARG;
+    if (!workspace || !aligned(workspace, 256) || workspace_bytes < filter_step_ws_bytes(n_traj, n_tokens))
+        return PACE_ERR_WORKSPACE;
+    double r_hat = *r_hat_inout;
+    int64_t budget = 0;
+    rc = pace_budget(occupancy, capacity, &p, &r_hat, &budget);
+    if (rc != PACE_OK) return rc;
+    const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
+    const bool use_prefix = prefix_score != nullptr && window_n >= wmin;
+    char *w = (char *)workspace;
+    const ScoreWorkspace sws = score_ws_carve(w, n_traj, n_tokens);
+    void *cws = w + align256(score_ws_bytes(n_traj, n_tokens));
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e = launch_score(tags, offsets, n_traj, n_tokens, completion, current_version, prefix_score,
+                                window_sorted, window_n, use_prefix, p.w_wait, p.gamma, score_out, gen_sum_out,
+                                gen_count_out, sws, aligned(tags, 16), st);
+    if (e == hipSuccess) {
+        const double rate = r_hat < p.r_max ? r_hat : p.r_max;
+        e = launch_stream_admit(score_out, n_traj, rate, p.window_min, batch_size, window_ring, window_cap,
+                                window_state, status_out, keep_out, reject_ids_out, kappa_out, counts_out, st);
+    }
+    if (e == hipSuccess)
+        e = launch_compact(offsets, n_traj, n_tokens, keep_out, cols, n_cols, offsets_out, kept_ids_out,
+                           n_kept_tokens_out, cws, st);
+    rc = hip_status(e);
+    if (rc != PACE_OK) return rc;
+    *r_hat_inout = r_hat;
+    return PACE_OK;
+}
+
 static_assert(PACE_PHASE_COUNT == kPhaseCount, "phase count");
 
 int pace_time_next_kernel(int phase, void *start_event, void *stop_event) {

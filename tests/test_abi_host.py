@@ -222,3 +222,22 @@ def test_stream_admit_host_argument_errors(L):
     assert call(ring=None) == -1
     assert call(state=None) == -1
     assert call(status=None) == -1
+
+
+def test_stream_step_host_argument_errors(L):
+    rh = ctypes.c_double(0.25)
+    cols = (ctypes.c_void_p * 1)(FAKE)
+    e4 = (ctypes.c_int32 * 1)(4)
+
+    def call(cap=512, B=10, ws=FAKE, wsb=1 << 30, ring=FAKE):
+        return L.pace_stream_step(FAKE, FAKE, 20, 100, FAKE, 10, None, None, 0, 30, 10, None, ctypes.byref(rh), B,
+                                  ring, cap, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, FAKE, FAKE, 1, cols, e4,
+                                  cols, FAKE, FAKE, FAKE, ws, wsb, None)
+
+    assert call(cap=0) == -1
+    assert call(cap=2048) == -1
+    assert call(B=-1) == -1
+    assert call(ring=None) == -1
+    assert call(ws=None) == -2
+    assert call(wsb=64) == -2
+    assert rh.value == 0.25

@@ -115,3 +115,42 @@ def test_stream_sweep_math_pool(pace):
         ost, okappa = check_step(pace, osc, rh_o, ow, gw, B)
         if step > 2:
             assert okappa < np.inf
+
+
+def test_stream_step_fused_matches_oracle(pace):
+    """pace_stream_step over 12 sweep steps of the math pool against the
+    oracle's score, budget, stream_admit and compact in sequence."""
+    pool = copy.deepcopy(poolgen.make_pool("math"))
+    V0 = pool.V
+    B = 200
+    ow = oracle.StreamWindow(512)
+    gw = pace.StreamWindow(512, DEV)
+    params = pace.default_params(beta=0.9, window_min=16)
+    rh_o = rh_g = 0.0
+    tags, off, comp, pre, win = D(pool.tags), D(pool.offsets), D(pool.completion), D(pool.prefix_score), D(pool.window)
+    bufs = None
+    for step in range(12):
+        slots = poolgen.sweep_step(pool, step, V0)
+        for i in slots:
+            lo, hi = int(pool.offsets[i]), int(pool.offsets[i + 1])
+            tags[lo:hi] = D(pool.tags[lo:hi])
+        comp.copy_(D(pool.completion))
+        pre.copy_(D(pool.prefix_score))
+        bufs, rh_g = pace.pace_stream_step(tags, off, comp, pool.V, pool.occupancy, pool.capacity, [tags], gw, B,
+                                           pre, win, params, rh_g, bufs)
+        torch.cuda.synchronize()
+        osc, oS, oT = oracle.score(pool.tags, pool.offsets, pool.completion, pool.V, pool.prefix_score, pool.window)
+        _, rh_o = oracle.budget(pool.occupancy, pool.capacity, rh_o, 0.9, 0.9)
+        ost, okappa, odrawn, okept = oracle.stream_admit(osc, rh_o, ow, B, window_min=16)
+        ooff, oids, opacked = oracle.compact(pool.offsets, (ost == 1).astype(np.uint8), [pool.tags])
+        say("stream step fused, sweep step %d drawn=%d kept=%d" % (step, odrawn, okept))
+        assert rh_g == rh_o
+        assert np.array_equal(H(bufs["score"])[: pool.n].view(np.uint64), osc.view(np.uint64))
+        assert np.array_equal(H(bufs["status"])[: pool.n], ost)
+        assert float(H(bufs["kappa"])[0]) == okappa
+        assert list(H(bufs["counts"])) == [odrawn, okept, odrawn - okept]
+        assert np.array_equal(H(gw.ring).view(np.uint64), ow.ring.view(np.uint64))
+        nk = int(H(bufs["n_kept_tokens"])[0])
+        assert np.array_equal(H(bufs["offsets_out"])[: okept + 1], ooff)
+        assert np.array_equal(H(bufs["kept_ids"])[:okept], oids)
+        assert np.array_equal(H(bufs["cols_out"][0])[:nk], opacked[0])
