@@ -54,8 +54,9 @@ def load_library(path: str):
     lib.oracle_group_score.argtypes = [P, i64, P, i64, P]
     lib.oracle_group_expand.argtypes = [P, i64, i64, P, P]
     lib.oracle_stream_admit.argtypes = [P, i64, d, d, i64, i64, P, i64, P, P, P, P, P, P]
+    lib.oracle_prefix_score.argtypes = [P, P, P, P, i64, i64, i64, i64, P]
     for f in ("oracle_validate", "oracle_score", "oracle_budget", "oracle_select", "oracle_compact",
-              "oracle_group_score", "oracle_group_expand", "oracle_stream_admit"):
+              "oracle_group_score", "oracle_group_expand", "oracle_stream_admit", "oracle_prefix_score"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -268,4 +269,21 @@ def stream_admit(score_arr, r_hat, window: StreamWindow, batch_size, r_max=0.9, 
         return rc
     window.head, window.count = int(head.value), int(cnt.value)
     return status[:n].copy(), float(kappa.value), int(drawn.value), int(kept.value)
+
+
+def prefix_score(lp_new, lp_behavior, prefix_offsets, tags=None, cap=1024, min_tokens=32, check=True):
+    """Eq. (5): mean |lp_new - lp_behavior| over each prefix's first `cap`
+    eligible tokens (tag != -1); NaN below `min_tokens` eligible tokens."""
+    a = _c(lp_new, np.float32)
+    b = _c(lp_behavior, np.float32)
+    po = _c(prefix_offsets, np.int64)
+    tg = None if tags is None else _c(tags, np.int32)
+    n = po.shape[0] - 1
+    out = np.empty(max(n, 1), np.float64)
+    rc = _load().oracle_prefix_score(_p(a), _p(b), _p(tg), _p(po), n, a.shape[0], int(cap), int(min_tokens), _p(out))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_prefix_score")
+        return rc
+    return out[:n].copy()
 

@@ -413,3 +413,45 @@ int oracle_stream_admit(const double *score, int64_t n, double r_hat, double r_m
     *n_retained_out = retained;
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------
+ * Prefix Forgetting Score (Eq. (5), Sec. 3.2; collection rules in
+ * Appendix B): the mean absolute difference between the rescoring policy's
+ * log-probabilities and the behaviour log-probabilities recorded during
+ * generation, over the rescored prefix's response tokens.
+ * Prefix i holds tokens [prefix_offsets[i], prefix_offsets[i+1]) of the
+ * packed arrays. Readings: a token tagged -1 (non-generated, tool output) is
+ * not eligible; only the first `cap` eligible tokens count (the scoring cap);
+ * a prefix with fewer than `min_tokens` eligible tokens gets no score (NaN);
+ * each term is |(double)lp_new - (double)lp_behavior| and the terms are
+ * added in token order in binary64, then divided once by their count.
+ * tags may be NULL (every token eligible).
+ * ---------------------------------------------------------------------- */
+int oracle_prefix_score(const float *lp_new, const float *lp_behavior, const int32_t *tags,
+                        const int64_t *prefix_offsets, int64_t n, int64_t n_tokens, int64_t cap,
+                        int64_t min_tokens, double *s_pre_out)
+{
+    if (n < 0 || n_tokens < 0 || cap < 0 || min_tokens < 0 || !prefix_offsets ||
+        (n > 0 && !s_pre_out) || (n_tokens > 0 && (!lp_new || !lp_behavior)))
+        return ORC_ERR_ARG;
+    if (prefix_offsets[0] != 0 || prefix_offsets[n] != n_tokens)
+        return ORC_ERR_PRECONDITION;
+    for (int64_t i = 0; i < n; i++)
+        if (prefix_offsets[i + 1] < prefix_offsets[i])
+            return ORC_ERR_PRECONDITION;
+    for (int64_t i = 0; i < n; i++) {
+        double sum = 0.0;
+        int64_t m = 0;
+        for (int64_t t = prefix_offsets[i]; t < prefix_offsets[i + 1]; t++) {
+            if (tags && tags[t] == -1)
+                continue;                /* non-generated token */
+            if (m == cap)
+                break;
+            double d = (double)lp_new[t] - (double)lp_behavior[t];
+            sum = sum + fabs(d);
+            m += 1;
+        }
+        s_pre_out[i] = (m >= min_tokens && m > 0) ? sum / (double)m : NAN;
+    }
+    return ORC_OK;
+}

@@ -66,14 +66,22 @@ MUTATIONS = [
      "for (int64_t i = 0; i < n && retained <= batch_size; i++) {"),
     ("stream window takes only retained scores", "        ring[head] = score[i];\n        head = (head + 1) % cap;",
      "        if (status_out[i] != 1) continue;\n        ring[head] = score[i];\n        head = (head + 1) % cap;"),
+    ("prefix score signed, not absolute", "sum = sum + fabs(d);", "sum = sum + d;"),
+    ("prefix cap ignored", "if (m == cap)\n                break;", "if (m == cap + 1000000)\n                break;"),
+    ("prefix masked tokens counted", "if (tags && tags[t] == -1)\n                continue;                /* non-generated token */",
+     "if (tags && tags[t] == -2)\n                continue;"),
+    ("prefix minimum not applied", "(m >= min_tokens && m > 0) ? sum / (double)m : NAN;", "(m > 0) ? sum / (double)m : NAN;"),
+    ("prefix mean over the span length", "sum / (double)m : NAN;",
+     "sum / (double)(prefix_offsets[i + 1] - prefix_offsets[i]) : NAN;"),
     ("stream window misses the newest entry", "sorted[t] = ring[(head - cnt + t + cap) % cap];",
      "sorted[t] = ring[(head - cnt + t + cap - 1) % cap];"),
 ]
 
 from tests import test_oracle_group_pins as group_pins
 from tests import test_oracle_stream_pins as stream_pins
+from tests import test_oracle_prefix_pins as prefix_pins
 
-PIN_FUNCS = [getattr(m, n) for m in (pins, group_pins, stream_pins) for n in dir(m)
+PIN_FUNCS = [getattr(m, n) for m in (pins, group_pins, stream_pins, prefix_pins) for n in dir(m)
              if n.startswith("test_") and callable(getattr(m, n))]
 
 
