@@ -310,6 +310,25 @@ int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
                      int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
                      void *workspace, size_t workspace_bytes, void *stream);
 
+/* pace_prefix_score -- Prefix Forgetting Score (Eq. (5), Sec. 3.2): for each
+ * rescored prefix, the mean absolute difference between the rescoring
+ * policy's log-probabilities and the behaviour log-probabilities recorded at
+ * generation, over the prefix's response tokens (Appendix B: only the first
+ * `cap` of them count -- 1024 for math, 2048 for tool use -- and a prefix
+ * needs at least `min_tokens` (32) of them, else it has no score).
+ * lp_new, lp_behavior: f32 [n_tokens], packed prefixes; prefix i holds tokens
+ *   [prefix_offsets[i], prefix_offsets[i+1]) (int64 [n+1], expected 0 ..
+ *   n_tokens non-decreasing; clamped on the device).
+ * tags: int32 [n_tokens] or NULL; a token tagged -1 is not a response token.
+ * s_pre_out: f64 [n]; NaN for a prefix without a score (pace_score then
+ *   applies no prefix weight, F = 1). Each term is formed in binary64 from the
+ *   two f32 values; the terms are added in a fixed tree order (bit-identical
+ *   run to run), which can differ from a sequential sum by a relative
+ *   (cap + 2) * 2^-53 at most. */
+int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32_t *tags,
+                      const int64_t *prefix_offsets, int64_t n, int64_t n_tokens, int64_t cap,
+                      int64_t min_tokens, double *s_pre_out, void *stream);
+
 /* pace_time_next_kernel -- measurement hook, not part of the method.
  * Arms a one-shot timer for one phase of the device work on the calling host
  * thread: the next kernel of that phase launched from this thread (by any

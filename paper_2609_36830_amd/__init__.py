@@ -423,6 +423,23 @@ def pace_stream_step(tags, offsets, completion, current_version, occupancy, capa
     return b, float(rh.value)
 
 
+def pace_prefix_score(lp_new, lp_behavior, prefix_offsets, tags=None, cap: int = 1024, min_tokens: int = 32,
+                      s_pre_out=None, stream=None):
+    """Eq. (5) per rescored prefix; NaN when fewer than min_tokens tokens count."""
+    _dev(lp_new, torch.float32, "lp_new")
+    _dev(lp_behavior, torch.float32, "lp_behavior")
+    _dev(prefix_offsets, torch.int64, "prefix_offsets")
+    if tags is not None:
+        _dev(tags, torch.int32, "tags")
+    n = prefix_offsets.numel() - 1
+    if s_pre_out is None:
+        s_pre_out = torch.empty(max(n, 1), dtype=torch.float64, device=lp_new.device)
+    _check(lib().pace_prefix_score(_ptr(lp_new), _ptr(lp_behavior), _ptr(tags), _ptr(prefix_offsets), n,
+                                   lp_new.numel(), int(cap), int(min_tokens), _ptr(s_pre_out),
+                                   _stream(lp_new.device, stream)), "pace_prefix_score")
+    return s_pre_out[:n]
+
+
 def pace_time_next_kernel(phase: int, start=None, stop=None):
     """Arm a one-shot timer on the next kernel of `phase` launched from this
     thread. start/stop are torch.cuda.Event(enable_timing=True) objects that

@@ -185,6 +185,11 @@ hipError_t launch_stream_admit(const double *score, int64_t n, double rate, int6
                                double *ring, int64_t cap, int64_t *state, uint8_t *status, uint8_t *keep,
                                int32_t *reject_ids, double *kappa, int64_t *counts, hipStream_t stream);
 
+// ---- Prefix Forgetting Score --------------------------------------------------
+hipError_t launch_prefix_score(const float *lp_new, const float *lp_beh, const int32_t *tags,
+                               const int64_t *prefix_offsets, int64_t n, int64_t n_tokens, int64_t cap,
+                               int64_t min_tokens, double *s_pre, hipStream_t stream);
+
 // ---- validate --------------------------------------------------------------
 hipError_t launch_validate(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                            const int32_t *completion, int32_t V, const double *window, int64_t W,

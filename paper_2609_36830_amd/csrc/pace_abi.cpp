@@ -431,6 +431,19 @@ int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
     return PACE_OK;
 }
 
+int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32_t *tags,
+                      const int64_t *prefix_offsets, int64_t n, int64_t n_tokens, int64_t cap,
+                      int64_t min_tokens, double *s_pre_out, void *stream) {
+    if (n < 0 || n >= INT32_MAX || n_tokens < 0 || cap < 0 || min_tokens < 0 || !prefix_offsets)
+        return PACE_ERR_INVALID_ARG;
+    if ((n > 0 && !s_pre_out) || (n_tokens > 0 && (!lp_new || !lp_behavior))) return PACE_ERR_INVALID_ARG;
+    if (!aligned(lp_new, 4) || !aligned(lp_behavior, 4) || !aligned(tags, 4) || !aligned(prefix_offsets, 8) ||
+        !aligned(s_pre_out, 8))
+        return PACE_ERR_INVALID_ARG;
+    return hip_status(launch_prefix_score(lp_new, lp_behavior, tags, prefix_offsets, n, n_tokens, cap, min_tokens,
+                                          s_pre_out, (hipStream_t)stream));
+}
+
 static_assert(PACE_PHASE_COUNT == kPhaseCount, "phase count");
 
 int pace_time_next_kernel(int phase, void *start_event, void *stop_event) {

@@ -297,3 +297,36 @@ def sweep_step(pool: Pool, step: int, V0: int, frac: float = 0.05, seed_base: in
         if pool.prefix_score is not None:
             pool.prefix_score[i] = np.nan
     return slots
+
+
+def make_prefixes(pool: Pool, seed: int = 0):
+    """Synthetic rescored prefixes for a pool: every trajectory with a version
+    break was interrupted there, and its prefix is its tokens before the first
+    break. Behaviour log-probabilities are drawn per token (f32, <= 0); the
+    rescoring policy's ones add a per-prefix drift. Returns (traj_ids,
+    prefix_offsets int64[m+1], lp_new f32, lp_behavior f32, tags int32)."""
+    rng = np.random.default_rng(seed + 4242)
+    ids, lens = [], []
+    for i in range(pool.n):
+        lo, hi = int(pool.offsets[i]), int(pool.offsets[i + 1])
+        t = pool.tags[lo:hi]
+        gen = np.flatnonzero(t != -1)
+        if len(gen) == 0:
+            continue
+        first = t[gen[0]]
+        later = gen[t[gen] != first]
+        if len(later) == 0:
+            continue
+        ids.append(i)
+        lens.append(int(later[0]))
+    ids = np.array(ids, np.int64)
+    po = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    m = int(po[-1])
+    tags = np.empty(m, np.int32)
+    for k, i in enumerate(ids):
+        lo = int(pool.offsets[i])
+        tags[po[k]:po[k + 1]] = pool.tags[lo:lo + lens[k]]
+    lp_b = np.minimum(rng.normal(-1.2, 0.8, m), 0.0).astype(np.float32)
+    drift = np.repeat(rng.lognormal(np.log(0.02), 1.0, len(ids)), lens)
+    lp_n = np.minimum(lp_b + rng.normal(0.0, 1.0, m) * drift, 0.0).astype(np.float32)
+    return ids, po, lp_n, lp_b, tags

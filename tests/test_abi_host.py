@@ -241,3 +241,13 @@ def test_stream_step_host_argument_errors(L):
     assert call(ws=None) == -2
     assert call(wsb=64) == -2
     assert rh.value == 0.25
+
+
+def test_prefix_score_host_argument_errors(L):
+    assert L.pace_prefix_score(FAKE, FAKE, None, None, 3, 10, 1024, 32, FAKE, None) == -1
+    assert L.pace_prefix_score(FAKE, FAKE, None, FAKE, -1, 10, 1024, 32, FAKE, None) == -1
+    assert L.pace_prefix_score(FAKE, FAKE, None, FAKE, 3, 10, -1, 32, FAKE, None) == -1
+    assert L.pace_prefix_score(FAKE, FAKE, None, FAKE, 3, 10, 1024, -1, FAKE, None) == -1
+    assert L.pace_prefix_score(None, FAKE, None, FAKE, 3, 10, 1024, 32, FAKE, None) == -1
+    assert L.pace_prefix_score(FAKE + 2, FAKE, None, FAKE, 3, 10, 1024, 32, FAKE, None) == -1
+    assert L.pace_prefix_score(FAKE, FAKE, None, FAKE, 3, 10, 1024, 32, None, None) == -1
