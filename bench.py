@@ -84,6 +84,43 @@ REDUCE_COUNTERS = {
 }
 
 
+def prefix_bench(pace, pool, K, flush, dev, stream, cap=1024, min_tokens=32):
+    """Prefix Forgetting Score (Eq. (5)) over the pool's synthetic rescored
+    prefixes (every trajectory with a version break, its tokens before the
+    first break), cold caches, kernel timed by its own events. Algorithmic
+    bytes: 12 B (two f32 log-probs and the tag) per token up to each prefix's
+    cap-th eligible token, plus 16 B of offsets and 8 B of output per prefix."""
+    import torch
+    import poolgen
+    ids, po, a, b, tg = poolgen.make_prefixes(pool, seed=0)
+    n = len(ids)
+    read = 0
+    for k in range(n):
+        elig = np.flatnonzero(tg[po[k]:po[k + 1]] != -1)
+        read += int(elig[cap - 1]) + 1 if len(elig) >= cap else int(po[k + 1] - po[k])
+    alg = 12 * read + 24 * n
+    Dt = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+    da, db, dp, dtg = Dt(a), Dt(b), Dt(po), Dt(tg)
+    out = torch.empty(max(n, 1), dtype=torch.float64, device=dev)
+    evs = []
+    for k in range(K + 2):
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record(stream)
+        ev[1].record(stream)
+        evs.append(ev)
+    torch.cuda.synchronize()
+    for k in range(K + 2):
+        flush.max()
+        pace.pace_time_next_kernel(pace.PHASE_PREFIX, *evs[k])
+        pace.pace_prefix_score(da, db, dp, dtg, cap, min_tokens, out)
+    torch.cuda.synchronize()
+    us = np.array([e[0].elapsed_time(e[1]) * 1e3 for e in evs[2:]])
+    t = float(us.mean()) * 1e-6
+    return {"entry": "pace_prefix_score", "prefixes": n, "prefix_tokens": int(po[-1]), "cap": cap,
+            "kernel_us_mean": float(us.mean()), "alg_bytes": alg, "achieved_GBps": alg / t / 1e9,
+            "hbm_frac_of_peak": alg / t / HBM_PEAK, "scored": int(np.isfinite(out[:n].cpu().numpy()).sum())}
+
+
 def stream_sweep(args, pace, pool, tags, off, comp, prefix, window, cols, dev, stream):
     """Back-to-back sweep with the streaming admission rule (no cache flush):
     per step s the current version is V0 + s and 5% of the slots are refreshed
@@ -301,6 +338,7 @@ def main():
 
     sweep = stream_sweep(args, pace, pool, tags, off, comp, prefix, window, cols, dev, stream) \
         if args.sweep_steps > 0 else None
+    prefix_res = prefix_bench(pace, pool, K, flush, dev, stream)
 
     if args.calib_copy:
         a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -349,6 +387,7 @@ def main():
         "kernel_us_p50": {k: float(np.median(v)) for k, v in kernel_us.items()},
         "warm_ms_per_step": warm_ms,
         "stream_sweep": sweep,
+        "prefix_score": prefix_res,
         "group_step": {
             "entry": "pace_group_filter_step (groups of 8, group mean score)",
             "n_groups": n_groups, "occupancy_groups": g_occ, "target_groups": g_cap,

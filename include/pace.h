@@ -336,9 +336,10 @@ int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32
  * events, so that hipEventElapsedTime(start, stop) afterwards gives that
  * kernel's own execution time. The launch consumes the timer.
  * phase: PACE_PHASE_REDUCE (token reduction of pace_score), PACE_PHASE_FINALIZE
- *   (score finalisation), PACE_PHASE_SELECT (the rank kernel, or the
- *   single-workgroup select of large pools), PACE_PHASE_COMPACT (the
- *   compaction copy kernel).
+ *   (score finalisation), PACE_PHASE_SELECT (the rank kernel, the
+ *   single-workgroup select of large pools, or the streaming draw),
+ *   PACE_PHASE_COMPACT (the compaction copy kernel), PACE_PHASE_PREFIX (the
+ *   Prefix Forgetting Score kernel).
  * start_event, stop_event: hipEvent_t handles created by the caller with
  *   timing enabled; both NULL disarms the phase. The caller keeps ownership.
  * Returns PACE_ERR_INVALID_ARG for an unknown phase or one NULL event. */
@@ -346,7 +347,8 @@ int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32
 #define PACE_PHASE_FINALIZE 1
 #define PACE_PHASE_SELECT 2
 #define PACE_PHASE_COMPACT 3
-#define PACE_PHASE_COUNT 4
+#define PACE_PHASE_PREFIX 4
+#define PACE_PHASE_COUNT 5
 int pace_time_next_kernel(int phase, void *start_event, void *stop_event);
 
 /* Static description of an error code. */
