@@ -55,8 +55,11 @@ def load_library(path: str):
     lib.oracle_group_expand.argtypes = [P, i64, i64, P, P]
     lib.oracle_stream_admit.argtypes = [P, i64, d, d, i64, i64, P, i64, P, P, P, P, P, P]
     lib.oracle_prefix_score.argtypes = [P, P, P, P, i64, i64, i64, i64, P]
+    lib.oracle_stale_k.argtypes = [P, P, i64, i64, P, i32, i64, P, P]
+    lib.oracle_diagnostics.argtypes = [P, P, i64, i64, P, i32, P, P, P, i64, P, P]
     for f in ("oracle_validate", "oracle_score", "oracle_budget", "oracle_select", "oracle_compact",
-              "oracle_group_score", "oracle_group_expand", "oracle_stream_admit", "oracle_prefix_score"):
+              "oracle_group_score", "oracle_group_expand", "oracle_stream_admit", "oracle_prefix_score",
+              "oracle_stale_k", "oracle_diagnostics"):
         getattr(lib, f).restype = ctypes.c_int
     return lib
 
@@ -286,4 +289,43 @@ def prefix_score(lp_new, lp_behavior, prefix_offsets, tags=None, cap=1024, min_t
             raise OracleError(rc, "oracle_prefix_score")
         return rc
     return out[:n].copy()
+
+
+def stale_k(tags, offsets, completion, V, k, check=True):
+    """Stale-k admission (Eq. (1) lag <= k). Returns (keep uint8[n], lag f64[n])."""
+    tags = _c(tags, np.int32)
+    offsets = _c(offsets, np.int64)
+    completion = _c(completion, np.int32)
+    n = offsets.shape[0] - 1
+    keep = np.empty(max(n, 1), np.uint8)
+    lag = np.empty(max(n, 1), np.float64)
+    rc = _load().oracle_stale_k(_p(tags), _p(offsets), n, tags.shape[0], _p(completion), int(V), int(k),
+                                _p(keep), _p(lag))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_stale_k")
+        return rc
+    return keep[:n].copy(), lag[:n].copy()
+
+
+def diagnostics(tags, offsets, completion, V, score_arr, keep, edges, check=True):
+    """Kept/rejected histograms of K_wait, K_gen, K_eff and exact totals.
+    edges: f64 [3][nbins+1]. Returns (hist int64[3][2][nbins+2], totals int64[2][4])."""
+    tags = _c(tags, np.int32)
+    offsets = _c(offsets, np.int64)
+    completion = _c(completion, np.int32)
+    s = _c(score_arr, np.float64)
+    kp = _c(keep, np.uint8)
+    e = _c(edges, np.float64)
+    nbins = e.shape[1] - 1
+    n = offsets.shape[0] - 1
+    hist = np.empty((3, 2, nbins + 2), np.int64)
+    tot = np.empty((2, 4), np.int64)
+    rc = _load().oracle_diagnostics(_p(tags), _p(offsets), n, tags.shape[0], _p(completion), int(V), _p(s),
+                                    _p(kp), _p(e), nbins, _p(hist), _p(tot))
+    if rc != OK:
+        if check:
+            raise OracleError(rc, "oracle_diagnostics")
+        return rc
+    return hist, tot
 

@@ -455,3 +455,104 @@ int oracle_prefix_score(const float *lp_new, const float *lp_behavior, const int
     }
     return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------
+ * Stale-k admission (Sec. 2, the controlled Stale-k setting): only
+ * trajectories whose policy lag, Eq. (1) -- the mean over response tokens of
+ * j - v_t -- is at most k are admitted. Computed from the tags as written:
+ * the integer sum of (j - v_t) over the response tokens against k T, so the
+ * comparison is exact. Reading: a trajectory without response tokens
+ * (T = 0) has no Generation Staleness and its lag is taken as j - c.
+ * lag_out (may be NULL) receives the lag as a double (sum / T, or j - c).
+ * ---------------------------------------------------------------------- */
+int oracle_stale_k(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                   const int32_t *completion, int32_t V, int64_t k, uint8_t *keep_out, double *lag_out)
+{
+    if (n < 0 || n_tokens < 0 || !offsets || (n > 0 && (!completion || !keep_out)) ||
+        (n_tokens > 0 && !tags))
+        return ORC_ERR_ARG;
+    int rc = oracle_validate(tags, offsets, n, n_tokens, completion, V);
+    if (rc != ORC_OK)
+        return rc;
+    for (int64_t i = 0; i < n; i++) {
+        int64_t lag_sum = 0, T = 0;
+        for (int64_t t = offsets[i]; t < offsets[i + 1]; t++) {
+            if (tags[t] == -1)
+                continue;
+            lag_sum += (int64_t)V - (int64_t)tags[t];
+            T += 1;
+        }
+        int64_t wait = (int64_t)V - (int64_t)completion[i];
+        if (T > 0) {
+            keep_out[i] = (lag_sum <= k * T) ? 1 : 0;
+            if (lag_out)
+                lag_out[i] = (double)lag_sum / (double)T;
+        } else {
+            keep_out[i] = (wait <= k) ? 1 : 0;
+            if (lag_out)
+                lag_out[i] = (double)wait;
+        }
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Admission diagnostics (Sec. 4, the staleness distribution diagnostics):
+ * histograms of Waiting, Generation and Effective Staleness over the
+ * candidates, split into retained and rejected, plus exact integer totals.
+ * Metric m of candidate i: K_wait = V - c, K_gen = S / T (0 when T = 0), and
+ * K_eff = score[i] (the admission score). Bin b of metric m holds values in
+ * [edges[m][b], edges[m][b+1]); values below edges[m][0] go to an underflow
+ * bin and values at or above edges[m][nbins] to an overflow bin.
+ * hist_out: int64 [3][2][nbins + 2], [metric][0 rejected, 1 retained][bin],
+ *   bin 0 = underflow, 1..nbins, nbins + 1 = overflow.
+ * totals_out: int64 [2][4], per class: count, sum of (V - c), sum S, sum T.
+ * ---------------------------------------------------------------------- */
+int oracle_diagnostics(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                       const int32_t *completion, int32_t V, const double *score, const uint8_t *keep,
+                       const double *edges, int64_t nbins, int64_t *hist_out, int64_t *totals_out)
+{
+    if (n < 0 || nbins < 1 || !offsets || !edges || !hist_out || !totals_out ||
+        (n > 0 && (!completion || !score || !keep)) || (n_tokens > 0 && !tags))
+        return ORC_ERR_ARG;
+    int rc = oracle_validate(tags, offsets, n, n_tokens, completion, V);
+    if (rc != ORC_OK)
+        return rc;
+    int64_t nb2 = nbins + 2;
+    memset(hist_out, 0, (size_t)(3 * 2 * nb2) * sizeof(int64_t));
+    memset(totals_out, 0, 8 * sizeof(int64_t));
+    for (int64_t i = 0; i < n; i++) {
+        int64_t c = completion[i], S = 0, T = 0;
+        for (int64_t t = offsets[i]; t < offsets[i + 1]; t++) {
+            if (tags[t] == -1)
+                continue;
+            S += c - (int64_t)tags[t];
+            T += 1;
+        }
+        double m[3];
+        m[0] = (double)((int64_t)V - c);
+        m[1] = (T > 0) ? (double)S / (double)T : 0.0;
+        m[2] = score[i];
+        int cls = keep[i] ? 1 : 0;
+        for (int q = 0; q < 3; q++) {
+            const double *e = edges + q * (nbins + 1);
+            int64_t bin;
+            if (!(m[q] >= e[0]))
+                bin = 0;
+            else if (m[q] >= e[nbins])
+                bin = nbins + 1;
+            else {
+                bin = 1;
+                while (!(m[q] < e[bin]))
+                    bin += 1;
+            }
+            hist_out[(q * 2 + cls) * nb2 + bin] += 1;
+        }
+        int64_t *tot = totals_out + cls * 4;
+        tot[0] += 1;
+        tot[1] += (int64_t)V - c;
+        tot[2] += S;
+        tot[3] += T;
+    }
+    return ORC_OK;
+}

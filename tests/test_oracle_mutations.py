@@ -73,6 +73,17 @@ MUTATIONS = [
     ("prefix minimum not applied", "(m >= min_tokens && m > 0) ? sum / (double)m : NAN;", "(m > 0) ? sum / (double)m : NAN;"),
     ("prefix mean over the span length", "sum / (double)m : NAN;",
      "sum / (double)(prefix_offsets[i + 1] - prefix_offsets[i]) : NAN;"),
+    ("stale-k strict comparison", "keep_out[i] = (lag_sum <= k * T) ? 1 : 0;", "keep_out[i] = (lag_sum < k * T) ? 1 : 0;"),
+    ("stale-k lag from completion, not current version", "lag_sum += (int64_t)V - (int64_t)tags[t];",
+     "lag_sum += (int64_t)completion[i] - (int64_t)tags[t];"),
+    ("stale-k empty trajectory admitted always", "keep_out[i] = (wait <= k) ? 1 : 0;", "keep_out[i] = 1;"),
+    ("stale-k masked tokens counted", "            if (tags[t] == -1)\n                continue;\n            lag_sum",
+     "            if (tags[t] == -2)\n                continue;\n            lag_sum"),
+    ("diagnostics bins closed on the right", "while (!(m[q] < e[bin]))", "while (!(m[q] <= e[bin]))"),
+    ("diagnostics classes swapped", "int cls = keep[i] ? 1 : 0;", "int cls = keep[i] ? 0 : 1;"),
+    ("diagnostics K_gen over all tokens", "m[1] = (T > 0) ? (double)S / (double)T : 0.0;",
+     "m[1] = (T > 0) ? (double)S / (double)(offsets[i + 1] - offsets[i]) : 0.0;"),
+    ("diagnostics totals miss T", "tot[3] += T;", "tot[3] += S;"),
     ("stream window misses the newest entry", "sorted[t] = ring[(head - cnt + t + cap) % cap];",
      "sorted[t] = ring[(head - cnt + t + cap - 1) % cap];"),
 ]
@@ -80,8 +91,9 @@ MUTATIONS = [
 from tests import test_oracle_group_pins as group_pins
 from tests import test_oracle_stream_pins as stream_pins
 from tests import test_oracle_prefix_pins as prefix_pins
+from tests import test_oracle_diag_pins as diag_pins
 
-PIN_FUNCS = [getattr(m, n) for m in (pins, group_pins, stream_pins, prefix_pins) for n in dir(m)
+PIN_FUNCS = [getattr(m, n) for m in (pins, group_pins, stream_pins, prefix_pins, diag_pins) for n in dir(m)
              if n.startswith("test_") and callable(getattr(m, n))]
 
 
