@@ -329,6 +329,33 @@ int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32
                       const int64_t *prefix_offsets, int64_t n, int64_t n_tokens, int64_t cap,
                       int64_t min_tokens, double *s_pre_out, void *stream);
 
+/* pace_stale_k -- the Stale-k admission rule (Sec. 2): a trajectory is
+ * admitted iff its policy lag, Eq. (1) (the mean over response tokens of
+ * j - v_t), is at most k. Exact: by Lemma 1 the lag is (S + (j - c) T) / T,
+ * compared as integers. A trajectory without response tokens (T = 0) has lag
+ * j - c.
+ * gen_sum, gen_count: int64 [n_traj] (pace_score's S and T); completion:
+ * int32 [n_traj]; current_version: j. k: 0 <= k < 2^31.
+ * keep_out: u8 [n_traj], 1 = admitted; lag_out: f64 [n_traj] or NULL. */
+int pace_stale_k(const int64_t *gen_sum, const int64_t *gen_count, const int32_t *completion,
+                 int32_t current_version, int64_t n_traj, int64_t k, uint8_t *keep_out, double *lag_out,
+                 void *stream);
+
+/* pace_diagnostics -- the admission diagnostics of Sec. 4: histograms of
+ * Waiting (K_wait = j - c), Generation (K_gen = S / T, 0 when T = 0) and
+ * Effective Staleness (the admission score) over the candidates, split into
+ * rejected (keep 0) and retained (keep != 0), and exact totals per class.
+ * score: f64 [n_traj]; gen_sum, gen_count: int64 [n_traj]; keep: u8 [n_traj].
+ * edges: f64 [3][nbins + 1] device, ascending per metric (K_wait, K_gen,
+ *   K_eff); 1 <= nbins <= 1024. Bin b holds [edges[b], edges[b+1]).
+ * hist_out: int64 [3][2][nbins + 2]: [metric][0 rejected, 1 retained][bin],
+ *   bin 0 below the first edge, nbins + 1 at or above the last.
+ * totals_out: int64 [2][4]: per class, count, sum of (j - c), sum S, sum T.
+ * One workgroup; outputs are overwritten, not accumulated. */
+int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t *gen_count,
+                     const int32_t *completion, int32_t current_version, const uint8_t *keep, int64_t n_traj,
+                     const double *edges, int nbins, int64_t *hist_out, int64_t *totals_out, void *stream);
+
 /* pace_time_next_kernel -- measurement hook, not part of the method.
  * Arms a one-shot timer for one phase of the device work on the calling host
  * thread: the next kernel of that phase launched from this thread (by any

@@ -440,6 +440,39 @@ def pace_prefix_score(lp_new, lp_behavior, prefix_offsets, tags=None, cap: int =
     return s_pre_out[:n]
 
 
+def pace_stale_k(gen_sum, gen_count, completion, current_version, k: int, keep_out=None, lag_out=None,
+                 with_lag=True, stream=None):
+    """Stale-k admission (Eq. (1) lag <= k). Returns (keep u8[n], lag f64[n] or None)."""
+    _dev(gen_sum, torch.int64, "gen_sum")
+    _dev(gen_count, torch.int64, "gen_count")
+    _dev(completion, torch.int32, "completion")
+    n = completion.numel()
+    dev = completion.device
+    keep_out = torch.empty(max(n, 1), dtype=torch.uint8, device=dev) if keep_out is None else keep_out
+    if with_lag and lag_out is None:
+        lag_out = torch.empty(max(n, 1), dtype=torch.float64, device=dev)
+    _check(lib().pace_stale_k(_ptr(gen_sum), _ptr(gen_count), _ptr(completion), int(current_version), n, int(k),
+                              _ptr(keep_out), _ptr(lag_out), _stream(dev, stream)), "pace_stale_k")
+    return keep_out[:n], (lag_out[:n] if lag_out is not None else None)
+
+
+def pace_diagnostics(score, gen_sum, gen_count, completion, current_version, keep, edges, hist_out=None,
+                     totals_out=None, stream=None):
+    """Kept/rejected staleness histograms. edges: f64 [3, nbins+1] device tensor.
+    Returns (hist int64 [3, 2, nbins+2], totals int64 [2, 4])."""
+    _dev(score, torch.float64, "score")
+    _dev(edges, torch.float64, "edges")
+    n = score.numel()
+    nbins = edges.shape[1] - 1
+    dev = score.device
+    hist_out = torch.empty((3, 2, nbins + 2), dtype=torch.int64, device=dev) if hist_out is None else hist_out
+    totals_out = torch.empty((2, 4), dtype=torch.int64, device=dev) if totals_out is None else totals_out
+    _check(lib().pace_diagnostics(_ptr(score), _ptr(gen_sum), _ptr(gen_count), _ptr(completion),
+                                  int(current_version), _ptr(keep), n, _ptr(edges), int(nbins), _ptr(hist_out),
+                                  _ptr(totals_out), _stream(dev, stream)), "pace_diagnostics")
+    return hist_out, totals_out
+
+
 def pace_time_next_kernel(phase: int, start=None, stop=None):
     """Arm a one-shot timer on the next kernel of `phase` launched from this
     thread. start/stop are torch.cuda.Event(enable_timing=True) objects that

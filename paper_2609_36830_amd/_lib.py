@@ -37,6 +37,8 @@ SIGNATURES = [
     ("pace_stream_step", ctypes.c_int, [P, P, i64, i64, P, i32, P, P, i64, i64, i64, P, P, i64, P, i64, P,
                                         P, P, P, P, P, P, P, P, ctypes.c_int, P, P, P, P, P, P, P, sz, P]),
     ("pace_prefix_score", ctypes.c_int, [P, P, P, P, i64, i64, i64, i64, P, P]),
+    ("pace_stale_k", ctypes.c_int, [P, P, P, i32, i64, i64, P, P, P]),
+    ("pace_diagnostics", ctypes.c_int, [P, P, P, P, i32, P, i64, P, ctypes.c_int, P, P, P]),
     ("pace_time_next_kernel", ctypes.c_int, [ctypes.c_int, P, P]),
     ("pace_strerror", ctypes.c_char_p, [ctypes.c_int]),
 ]

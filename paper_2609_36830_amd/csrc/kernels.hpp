@@ -190,6 +190,14 @@ hipError_t launch_prefix_score(const float *lp_new, const float *lp_beh, const i
                                const int64_t *prefix_offsets, int64_t n, int64_t n_tokens, int64_t cap,
                                int64_t min_tokens, double *s_pre, hipStream_t stream);
 
+// ---- Stale-k admission and diagnostics ----------------------------------------
+constexpr int kDiagBinsMax = 1024;
+hipError_t launch_stale_k(const int64_t *S, const int64_t *T, const int32_t *completion, int32_t V, int64_t n,
+                          int64_t k, uint8_t *keep, double *lag, hipStream_t stream);
+hipError_t launch_diagnostics(const double *score, const int64_t *S, const int64_t *T, const int32_t *completion,
+                              int32_t V, const uint8_t *keep, int64_t n, const double *edges, int nbins,
+                              int64_t *hist, int64_t *totals, hipStream_t stream);
+
 // ---- validate --------------------------------------------------------------
 hipError_t launch_validate(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                            const int32_t *completion, int32_t V, const double *window, int64_t W,

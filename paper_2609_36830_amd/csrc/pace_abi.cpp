@@ -444,6 +444,32 @@ int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32
                                           s_pre_out, (hipStream_t)stream));
 }
 
+int pace_stale_k(const int64_t *gen_sum, const int64_t *gen_count, const int32_t *completion,
+                 int32_t current_version, int64_t n_traj, int64_t k, uint8_t *keep_out, double *lag_out,
+                 void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || k < 0 || k >= INT32_MAX || current_version < 0)
+        return PACE_ERR_INVALID_ARG;
+    if (n_traj > 0 && (!gen_sum || !gen_count || !completion || !keep_out)) return PACE_ERR_INVALID_ARG;
+    if (!aligned(gen_sum, 8) || !aligned(gen_count, 8) || !aligned(completion, 4) || !aligned(lag_out, 8))
+        return PACE_ERR_INVALID_ARG;
+    return hip_status(launch_stale_k(gen_sum, gen_count, completion, current_version, n_traj, k, keep_out, lag_out,
+                                     (hipStream_t)stream));
+}
+
+int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t *gen_count,
+                     const int32_t *completion, int32_t current_version, const uint8_t *keep, int64_t n_traj,
+                     const double *edges, int nbins, int64_t *hist_out, int64_t *totals_out, void *stream) {
+    if (n_traj < 0 || n_traj >= INT32_MAX || nbins < 1 || nbins > kDiagBinsMax || current_version < 0)
+        return PACE_ERR_INVALID_ARG;
+    if (!edges || !hist_out || !totals_out) return PACE_ERR_INVALID_ARG;
+    if (n_traj > 0 && (!score || !gen_sum || !gen_count || !completion || !keep)) return PACE_ERR_INVALID_ARG;
+    if (!aligned(score, 8) || !aligned(gen_sum, 8) || !aligned(gen_count, 8) || !aligned(completion, 4) ||
+        !aligned(edges, 8) || !aligned(hist_out, 8) || !aligned(totals_out, 8))
+        return PACE_ERR_INVALID_ARG;
+    return hip_status(launch_diagnostics(score, gen_sum, gen_count, completion, current_version, keep, n_traj,
+                                         edges, nbins, hist_out, totals_out, (hipStream_t)stream));
+}
+
 static_assert(PACE_PHASE_COUNT == kPhaseCount, "phase count");
 
 int pace_time_next_kernel(int phase, void *start_event, void *stop_event) {

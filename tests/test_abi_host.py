@@ -251,3 +251,14 @@ def test_prefix_score_host_argument_errors(L):
     assert L.pace_prefix_score(None, FAKE, None, FAKE, 3, 10, 1024, 32, FAKE, None) == -1
     assert L.pace_prefix_score(FAKE + 2, FAKE, None, FAKE, 3, 10, 1024, 32, FAKE, None) == -1
     assert L.pace_prefix_score(FAKE, FAKE, None, FAKE, 3, 10, 1024, 32, None, None) == -1
+
+
+def test_stale_k_and_diagnostics_host_argument_errors(L):
+    assert L.pace_stale_k(FAKE, FAKE, FAKE, 10, 5, -1, FAKE, None, None) == -1
+    assert L.pace_stale_k(FAKE, FAKE, FAKE, 10, 5, 2 ** 31, FAKE, None, None) == -1
+    assert L.pace_stale_k(None, FAKE, FAKE, 10, 5, 3, FAKE, None, None) == -1
+    assert L.pace_stale_k(FAKE, FAKE, FAKE, 10, 5, 3, None, None, None) == -1
+    assert L.pace_diagnostics(FAKE, FAKE, FAKE, FAKE, 10, FAKE, 5, FAKE, 0, FAKE, FAKE, None) == -1
+    assert L.pace_diagnostics(FAKE, FAKE, FAKE, FAKE, 10, FAKE, 5, FAKE, 1025, FAKE, FAKE, None) == -1
+    assert L.pace_diagnostics(FAKE, FAKE, FAKE, FAKE, 10, FAKE, 5, None, 8, FAKE, FAKE, None) == -1
+    assert L.pace_diagnostics(FAKE, FAKE, FAKE, FAKE, 10, None, 5, FAKE, 8, FAKE, FAKE, None) == -1
