@@ -84,6 +84,41 @@ REDUCE_COUNTERS = {
 }
 
 
+def aux_bench(pace, pool, step, off, comp, K, flush, dev, stream):
+    """Cold-cache kernel times (own events) of the single-kernel calls that
+    follow a step: Stale-k admission (k = 8) and the admission diagnostics
+    (64 bins per metric), on the last step's scores and keep flags."""
+    import torch
+    n = pool.n
+    S, T, sc, keep = step.gen_sum[:n], step.gen_count[:n], step.score[:n], step.keep[:n]
+    edges = torch.stack([torch.linspace(0, 16, 65, dtype=torch.float64, device=dev)] * 3)
+    skeep = torch.empty(n, dtype=torch.uint8, device=dev)
+    lag = torch.empty(n, dtype=torch.float64, device=dev)
+    hist = torch.empty((3, 2, 66), dtype=torch.int64, device=dev)
+    tot = torch.empty((2, 4), dtype=torch.int64, device=dev)
+    calls = {
+        "stale_k": lambda: pace.pace_stale_k(S, T, comp, pool.V, 8, skeep, lag),
+        "diagnostics": lambda: pace.pace_diagnostics(sc, S, T, comp, pool.V, keep, edges, hist, tot),
+    }
+    res = {}
+    for name, fn in calls.items():
+        evs = []
+        for k in range(K + 2):
+            ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            ev[0].record(stream)
+            ev[1].record(stream)
+            evs.append(ev)
+        torch.cuda.synchronize()
+        for k in range(K + 2):
+            flush.max()
+            pace.pace_time_next_kernel(pace.PHASE_AUX, *evs[k])
+            fn()
+        torch.cuda.synchronize()
+        res[name + "_us_mean"] = float(np.mean([e[0].elapsed_time(e[1]) * 1e3 for e in evs[2:]]))
+    res["stale_k_admitted"] = int(skeep.sum().item())
+    return res
+
+
 def prefix_bench(pace, pool, K, flush, dev, stream, cap=1024, min_tokens=32):
     """Prefix Forgetting Score (Eq. (5)) over the pool's synthetic rescored
     prefixes (every trajectory with a version break, its tokens before the
@@ -339,6 +374,7 @@ def main():
     sweep = stream_sweep(args, pace, pool, tags, off, comp, prefix, window, cols, dev, stream) \
         if args.sweep_steps > 0 else None
     prefix_res = prefix_bench(pace, pool, K, flush, dev, stream)
+    aux_res = aux_bench(pace, pool, step, off, comp, K, flush, dev, stream)
 
     if args.calib_copy:
         a = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
@@ -388,6 +424,7 @@ def main():
         "warm_ms_per_step": warm_ms,
         "stream_sweep": sweep,
         "prefix_score": prefix_res,
+        "aux_kernels": aux_res,
         "group_step": {
             "entry": "pace_group_filter_step (groups of 8, group mean score)",
             "n_groups": n_groups, "occupancy_groups": g_occ, "target_groups": g_cap,

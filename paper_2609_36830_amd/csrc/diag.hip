@@ -97,14 +97,14 @@ __global__ __launch_bounds__(kDT) void diagnostics_kernel(
 hipError_t launch_stale_k(const int64_t *S, const int64_t *T, const int32_t *completion, int32_t V, int64_t n,
                           int64_t k, uint8_t *keep, double *lag, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    return launch(-1, stale_k_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), stream, S, T, completion, V, n,
+    return launch(kPhaseAux, stale_k_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), stream, S, T, completion, V, n,
                   k, keep, lag);
 }
 
 hipError_t launch_diagnostics(const double *score, const int64_t *S, const int64_t *T, const int32_t *completion,
                               int32_t V, const uint8_t *keep, int64_t n, const double *edges, int nbins,
                               int64_t *hist, int64_t *totals, hipStream_t stream) {
-    return launch(-1, diagnostics_kernel, dim3(1), dim3(kDT), stream, score, S, T, completion, V, keep, n, edges,
+    return launch(kPhaseAux, diagnostics_kernel, dim3(1), dim3(kDT), stream, score, S, T, completion, V, keep, n, edges,
                   nbins, hist, totals);
 }
 

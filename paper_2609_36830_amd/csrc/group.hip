@@ -57,14 +57,14 @@ __global__ __launch_bounds__(256) void group_validate_kernel(const int64_t *__re
 hipError_t launch_group_score(const double *score, int64_t n, const int64_t *group_offsets, int64_t ng,
                               double *group_score, hipStream_t stream) {
     if (ng == 0) return hipSuccess;
-    return launch(-1, group_score_kernel, dim3((unsigned)((ng + 255) / 256)), dim3(256), stream, score, n,
+    return launch(kPhaseAux, group_score_kernel, dim3((unsigned)((ng + 255) / 256)), dim3(256), stream, score, n,
                   group_offsets, ng, group_score);
 }
 
 hipError_t launch_group_expand(const int64_t *group_offsets, int64_t ng, int64_t n, const uint8_t *group_keep,
                                uint8_t *keep, hipStream_t stream) {
     if (ng == 0 || n == 0) return hipSuccess;
-    return launch(-1, group_expand_kernel, dim3((unsigned)((ng + 3) / 4)), dim3(256), stream, group_offsets,
+    return launch(kPhaseAux, group_expand_kernel, dim3((unsigned)((ng + 3) / 4)), dim3(256), stream, group_offsets,
                   ng, n, group_keep, keep);
 }
 
