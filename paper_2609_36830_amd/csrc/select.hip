@@ -211,7 +211,7 @@ __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__
                                                      const int64_t *__restrict__ off, int64_t NT,
                                                      PieceParts parts) {
     __shared__ uint64_t tile[kRankTile];
-    __shared__ uint32_t part[kRankS][kRankQ + 1];
+    __shared__ uint32_t part[kRankT / kWave][kRankQ + 1];
     const int t = threadIdx.x;
     const int q = t % kRankQ, s = t / kRankQ;
     const int32_t i = (int32_t)((int64_t)blockIdx.x * kRankQ + q);
@@ -226,7 +226,19 @@ __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__
     for (int64_t b0 = 0; b0 < n; b0 += kRankTile) {
         const int m = (int)((n - b0) < kRankTile ? (n - b0) : kRankTile);
         __syncthreads();
-        for (int x = t; x < m; x += kRankT) tile[x] = score_key(score[b0 + x]);
+        // all of a thread's loads in flight at once, then the keys
+        constexpr int kPer = kRankTile / kRankT;
+        double v[kPer];
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int x = t + u * kRankT;
+            v[u] = x < m ? score[b0 + x] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int x = t + u * kRankT;
+            if (x < m) tile[x] = score_key(v[u]);
+        }
         __syncthreads();
         const int32_t jb = (int32_t)b0;
         int x = s;
@@ -243,14 +255,20 @@ __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__
             cnt += (kj > ki || (kj == ki && jb + x < i)) ? 1u : 0u;
         }
     }
-    part[s][q] = cnt;
+    // A wave holds four slices of every target (lane = slice * 16 + target):
+    // add them with two butterflies, then the 16 waves' sums through LDS.
+    static_assert(kRankQ * 4 == kWave, "four slices per wave");
+    cnt += (uint32_t)__shfl_xor((int)cnt, kRankQ, kWave);
+    cnt += (uint32_t)__shfl_xor((int)cnt, 2 * kRankQ, kWave);
+    if ((t % kWave) < kRankQ) part[t / kWave][q] = cnt;
     __syncthreads();
     if (t < kWave) {   // wave 0; lanes below kRankQ own the targets
         const int64_t ii = (int64_t)blockIdx.x * kRankQ + t;
         bool kept = false;
         if (t < kRankQ && ii < n) {
             uint32_t r = 0;
-            for (int k = 0; k < kRankS; ++k) r += part[k][t];
+#pragma unroll
+            for (int k = 0; k < kRankT / kWave; ++k) r += part[k][t];
             kept = (int64_t)r >= budget;
             keep[ii] = kept ? 1 : 0;
         }
