@@ -53,11 +53,13 @@ struct BoundCache {
     }
 };
 
+// Tags are >= -1, so (tag + 1) summed is the tags' sum plus 4 (mod 2^32; the
+// true partial stays below 2^32), and a tag is masked exactly when its sign
+// bit is set.
 __device__ __forceinline__ void add_all(const int4 &v, uint32_t &s, uint32_t &c) {
-    uint32_t u0 = (uint32_t)v.x + 1u, u1 = (uint32_t)v.y + 1u;
-    uint32_t u2 = (uint32_t)v.z + 1u, u3 = (uint32_t)v.w + 1u;
-    s += u0 + u1 + u2 + u3;
-    c += (u0 != 0u) + (u1 != 0u) + (u2 != 0u) + (u3 != 0u);
+    const uint32_t x0 = (uint32_t)v.x, x1 = (uint32_t)v.y, x2 = (uint32_t)v.z, x3 = (uint32_t)v.w;
+    s += x0 + x1 + x2 + x3 + 4u;
+    c += 4u - ((x0 >> 31) + (x1 >> 31) + (x2 >> 31) + (x3 >> 31));
 }
 
 __device__ __forceinline__ void add_all_wide(const int4 &v, uint64_t &s, uint32_t &c) {
