@@ -41,6 +41,10 @@ hipError_t launch(int phase, void (*kernel)(P...), dim3 grid, dim3 block, hipStr
 }
 
 // ---- score: segmented reduction over token chunks --------------------------
+// Waves per CU the reduction is sized for (its register use, at most 128
+// VGPRs, keeps that many resident; 32 per CU would force spills and was
+// measured much slower).
+constexpr int kReduceWavesPerCU = 16;
 // One wave reduces one chunk of consecutive tokens; the chunk length is a
 // multiple of kScoreChunkAlign chosen so that the chunks fill the device once.
 constexpr int64_t kScoreChunkAlign = 2048;

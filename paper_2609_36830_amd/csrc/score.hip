@@ -34,6 +34,7 @@ namespace {
 constexpr int kVec = 4;                       // tags per lane per window
 constexpr int kWin = kWave * kVec;            // 256 tokens per wave window
 constexpr int kUnroll = 4;                    // windows per super-window
+constexpr int kSub = 4;                       // windows per fast-path / walk block
 constexpr bool kDoubleBuffer = false;         // two super-windows in flight
 constexpr int kWavesPerBlock = 4;
 static_assert(kScoreChunkAlign % (kWin * kUnroll) == 0, "chunk must be a multiple of the super-window");
@@ -187,46 +188,30 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
         acc_c = 0;
     };
 
-    // Adds the super-window at `pos` (held in v) to the running pieces.
-    auto process = [&](int4 (&v)[U], int64_t pos) {
-        const int64_t send = (pos + kSuper < ce) ? pos + kSuper : ce;
-        if (valid && cur_end >= send) {
-            // Fast path: the whole super-window lies in trajectory `cur`.
-            if (kNarrow) {
-                uint32_t s32 = 0, c32 = 0;
-#pragma unroll
-                for (int k = 0; k < U; ++k) add_all(v[k], s32, c32);
-                acc_s += s32;
-                acc_c += c32;
-            } else {
-#pragma unroll
-                for (int k = 0; k < U; ++k) add_all_wide(v[k], acc_s, acc_c);
-            }
-            return;
-        }
-        // Boundary path: the super-window holds trajectory ends. Walk them
-        // in order; for each trajectory piece every lane adds its tags whose
-        // positions fall in the piece.
-        int64_t lo = pos;
+    // Boundary walk over the kSub vectors at vb (tokens [bpos, bend)): walk
+    // the trajectory ends in order; for each trajectory piece every lane adds
+    // its tags whose positions fall in the piece.
+    auto walk = [&](int4 *vb, int64_t bpos, int64_t bend) {
+        int64_t lo = bpos;
         while (true) {
-            const int64_t hi = cur_end < send ? cur_end : send;
+            const int64_t hi = cur_end < bend ? cur_end : bend;
             if (valid && hi > lo) {
                 // Keep the per-tag work inside this loop: hoisted out of it,
                 // it would hold every tag's (tag + 1) live at once.
 #pragma unroll
-                for (int k = 0; k < U; ++k)
-                    asm volatile("" : "+v"(v[k].x), "+v"(v[k].y), "+v"(v[k].z), "+v"(v[k].w));
-                // Positions relative to the super-window fit in 32 bits.
-                const uint32_t rlo = (uint32_t)(lo - pos), rlen = (uint32_t)(hi - lo);
+                for (int k = 0; k < kSub; ++k)
+                    asm volatile("" : "+v"(vb[k].x), "+v"(vb[k].y), "+v"(vb[k].z), "+v"(vb[k].w));
+                // Positions relative to the block fit in 32 bits.
+                const uint32_t rlo = (uint32_t)(lo - bpos), rlen = (uint32_t)(hi - lo);
                 uint64_t ps = 0;
                 uint32_t pc = 0;
 #pragma unroll
-                for (int k = 0; k < U; ++k)
-                    add_range(v[k], (uint32_t)(k * kWin + lane * kVec), rlo, rlen, ps, pc);
+                for (int k = 0; k < kSub; ++k)
+                    add_range(vb[k], (uint32_t)(k * kWin + lane * kVec), rlo, rlen, ps, pc);
                 acc_s += ps;
                 acc_c += pc;
             }
-            if (cur_end > send) break;            // trajectory continues past this super-window
+            if (cur_end > bend) break;            // trajectory continues past this block
             if (pending) flush();                 // trajectory `cur` ends at cur_end
             lo = cur_end;
             ++cur;
@@ -241,7 +226,35 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
                 cur_end = bc.get(off, n, NT, cur + 1);
                 pending = lo < ce;
             }
-            if (lo >= send) break;
+            if (lo >= bend) break;
+        }
+    };
+
+    // Adds the kSub vectors at vb (all inside trajectory `cur`).
+    auto add_block = [&](const int4 *vb) {
+        if (kNarrow) {
+            uint32_t s32 = 0, c32 = 0;
+#pragma unroll
+            for (int k = 0; k < kSub; ++k) add_all(vb[k], s32, c32);
+            acc_s += s32;
+            acc_c += c32;
+        } else {
+#pragma unroll
+            for (int k = 0; k < kSub; ++k) add_all_wide(vb[k], acc_s, acc_c);
+        }
+    };
+
+    // Adds the super-window at `pos` (held in v) to the running pieces: whole
+    // blocks of kSub vectors inside trajectory `cur` take the fast path, a
+    // block holding a trajectory end is walked.
+    auto process = [&](int4 (&v)[U], int64_t pos) {
+#pragma unroll
+        for (int h = 0; h < U / kSub; ++h) {
+            const int64_t bpos = pos + (int64_t)h * kSub * kWin;
+            if (bpos >= ce) break;
+            const int64_t bend = (bpos + kSub * kWin < ce) ? bpos + kSub * kWin : ce;
+            if (valid && cur_end >= bend) add_block(v + h * kSub);
+            else walk(v + h * kSub, bpos, bend);
         }
     };
 
@@ -309,7 +322,7 @@ hipError_t launch_score_reduce(const int32_t *tags, const int64_t *offsets, int6
                                hipStream_t stream, int64_t *chunk_len_out) {
     // One contiguous, equal token range per resident wave: a single balanced
     // round with no tail of late workgroups.
-    const int64_t chunk_len = score_chunk_len(n_tokens, resident_waves());
+    const int64_t chunk_len = score_chunk_len(n_tokens, resident_waves() / 16 * kReduceWavesPerCU);
     *chunk_len_out = chunk_len;
     const int64_t ch = n_tokens > 0 ? (n_tokens + chunk_len - 1) / chunk_len : 0;
     if (n == 0 || ch == 0) return hipSuccess;
