@@ -282,18 +282,30 @@ __global__ __launch_bounds__(256) void score_finalize_kernel(
     int use_prefix, double w_wait, int gamma, int64_t chunk_len, ScoreWorkspace ws,
     double *__restrict__ score, int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count) {
     __shared__ double win_lds[kWinLds ? kWindowLdsMax : 1];
+    // The trajectory's own loads go first (they do not wait for the window),
+    // then the window is staged; every thread reaches the barrier.
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const bool in = i < n;
+    int64_t lo = 0, hi = 0;
+    int32_t c = 0;
+    double s_pre = 0.0;
+    if (in) {
+        lo = clamp64(off[i], 0, NT);
+        hi = clamp64(off[i + 1], 0, NT);
+        c = completion[i];
+        if (use_prefix) s_pre = prefix[i];
+    }
+    const TrajPieces pc = in ? gather_pieces(i, lo, hi, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt,
+                                             chunk_len)
+                             : TrajPieces{0, 0};
     if (kWinLds && use_prefix) {
+#pragma unroll 4
         for (int64_t k = threadIdx.x; k < W; k += blockDim.x) win_lds[k] = window[k];
         __syncthreads();
     }
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    const int64_t lo = clamp64(off[i], 0, NT), hi = clamp64(off[i + 1], 0, NT);
-    const TrajPieces pc = gather_pieces(i, lo, hi, ws.part_sum, ws.part_cnt, ws.carry_sum,
-                                        ws.carry_cnt, chunk_len);
-    const TrajScore r = score_from_pieces(pc, completion[i], V, use_prefix != 0,
-                                          use_prefix ? prefix[i] : 0.0, kWinLds ? win_lds : window,
-                                          W, w_wait, gamma);
+    if (!in) return;
+    const TrajScore r = score_from_pieces(pc, c, V, use_prefix != 0, s_pre, kWinLds ? win_lds : window, W,
+                                          w_wait, gamma);
     score[i] = r.score;
     if (gen_sum) gen_sum[i] = r.S;
     if (gen_count) gen_count[i] = r.T;
