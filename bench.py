@@ -80,8 +80,8 @@ def reduce_traffic(config):
 
 # config -> {"sha256": digest of the score_reduce sources, "bytes": HBM bytes per launch}
 REDUCE_COUNTERS = {
-    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98115.5 KiB, WRITE_SIZE 273.7 KiB
-    "stress": {"sha256": "7784683db2f83137ed858820ca0f9134061992691cb1499722615668dfae9ce3", "bytes": 201220813},
+    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98114.2 KiB, WRITE_SIZE 264.5 KiB
+    "stress": {"sha256": "773337b866379c7e6d732d0d3ffbe61dccd6da6e9a28f12577342305480fe729", "bytes": 201208730},
 }
 
 
