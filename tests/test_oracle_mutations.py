@@ -19,7 +19,8 @@ MUTATIONS = [
     ("waiting term dropped", "score_out[i] = wait_term + gen_term;", "score_out[i] = gen_term;"),
     ("waiting staleness sign flipped", "double K_wait = (double)((int64_t)V - c);",
      "double K_wait = (double)(c - (int64_t)V);"),
-    ("K_gen operands transposed", "(double)S / (double)T : 0.0", "(double)T / ((double)S + 1.0) : 0.0"),
+    ("K_gen operands transposed", "double K_gen = (T > 0) ? (double)S / (double)T : 0.0;",
+     "double K_gen = (T > 0) ? (double)T / ((double)S + 1.0) : 0.0;"),
     ("phi numerator transposed", "F = (double)A / (double)(A + B);", "F = (double)B / (double)(A + B);"),
     ("ECDF strict instead of <=", "if (window[k] <= prefix[i])", "if (window[k] < prefix[i])"),
     ("gamma ignored on complement", "int64_t B = ipow(W - a, gamma);", "int64_t B = ipow(W - a, 1);"),
