@@ -6,9 +6,11 @@ stress pool: 4096 trajectories, log-normal lengths around 12k tokens up to
 32768 (50.1M int32 version tags), 0-16 version breaks each, V = 5000,
 occupancy 3x the target (budget 2731), scored with Effective Staleness
 (prefix window of 512, gamma 4), one int32 payload column (the tags)
-compacted into the batch. Inputs are resident in HBM before timing; before
-every timed step the L2 and MALL are flushed by reading a 512 MiB buffer
-(outside the timed events), so each step starts from cold caches.
+compacted into the batch. Inputs are resident in HBM before timing. The
+headline times K steps back to back between one event pair, over three copies
+of the pool used in rotation: one step moves more bytes than the 256 MB MALL
+holds, so each step starts with its pool copy out of the caches. The same
+steps are also timed one by one after an explicit 512 MiB cache flush.
 
 Prints ONE JSON line. Usage: python bench.py [--steps K] [--warmup W]
 """
