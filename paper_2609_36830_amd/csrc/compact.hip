@@ -331,54 +331,64 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
         return;
     }
 
-    // 2b. Piece pq: its block, then its trajectory within the block.
-    const int64_t pq = q - nb;
-    if (pq >= (int64_t)tot_p) return;
+    // 2b. Pieces q - nb, q - nb + stride, ... (stride = piece workgroups in
+    //     the grid): for each, its block, then its trajectory in the block.
+    const int64_t stride = (int64_t)gridDim.x - nb;
+    for (int64_t pq = q - nb; pq < (int64_t)tot_p; pq += stride) {
+        __syncthreads();                       // the previous piece's reads of sel/piece are done
+        if (t == 0) {
+            sel[0] = sel[1] = sel[2] = 0;
+            piece[0] = piece[1] = piece[2] = 0;   // an unmatched piece copies nothing
+        }
+        __syncthreads();
+        uint32_t pbk = pb;
+        int64_t lbk = lb;
 #pragma unroll
-    for (int k = 0; k < kPartsPerThread; ++k) {
-        const int64_t b = (int64_t)t * kPartsPerThread + k;
-        if (b < nb && pc[k] > 0 && (int64_t)pb <= pq && pq < (int64_t)pb + pc[k]) {
-            sel[0] = b;
-            sel[1] = pb;
-            sel[2] = lb;
+        for (int k = 0; k < kPartsPerThread; ++k) {
+            const int64_t b = (int64_t)t * kPartsPerThread + k;
+            if (b < nb && pc[k] > 0 && (int64_t)pbk <= pq && pq < (int64_t)pbk + pc[k]) {
+                sel[0] = b;
+                sel[1] = pbk;
+                sel[2] = lbk;
+            }
+            pbk += pc[k];
+            lbk += l[k];
         }
-        pb += pc[k];
-        lb += l[k];
-    }
-    __syncthreads();
-    if (t < kWave) {
-        const int64_t b = sel[0];
-        const int64_t i = b * kPieceBlock + t;
-        int64_t len = 0, lo = 0;
-        if (t < kPieceBlock && i < n) {
-            const int64_t k = kept_span(off, keep, i, NT, lo);
-            len = k > 0 ? k : 0;
+        __syncthreads();
+        if (t < kWave) {
+            const int64_t b = sel[0];
+            const int64_t i = b * kPieceBlock + t;
+            int64_t len = 0, lo = 0;
+            if (t < kPieceBlock && i < n) {
+                const int64_t k = kept_span(off, keep, i, NT, lo);
+                len = k > 0 ? k : 0;
+            }
+            const int64_t np = (len + kPieceLen - 1) / kPieceLen;
+            const int64_t np_incl = wave_incl_scan_i64(np);
+            const int64_t len_incl = wave_incl_scan_i64(len);
+            const int64_t qq = pq - sel[1];
+            if (np > 0 && np_incl - np <= qq && qq < np_incl) {
+                const int64_t k = qq - (np_incl - np);
+                piece[0] = sel[2] + (len_incl - len) + k * kPieceLen;
+                piece[1] = lo + k * kPieceLen;
+                piece[2] = (len - k * kPieceLen) < kPieceLen ? len - k * kPieceLen : kPieceLen;
+            }
         }
-        const int64_t np = (len + kPieceLen - 1) / kPieceLen;
-        const int64_t np_incl = wave_incl_scan_i64(np);
-        const int64_t len_incl = wave_incl_scan_i64(len);
-        const int64_t qq = pq - sel[1];
-        if (np > 0 && np_incl - np <= qq && qq < np_incl) {
-            const int64_t k = qq - (np_incl - np);
-            piece[0] = sel[2] + (len_incl - len) + k * kPieceLen;
-            piece[1] = lo + k * kPieceLen;
-            piece[2] = (len - k * kPieceLen) < kPieceLen ? len - k * kPieceLen : kPieceLen;
-        }
-    }
-    __syncthreads();
-    const int64_t d = piece[0], s = piece[1];
-    int64_t m = piece[2];
-    if (d >= NT || m <= 0) return;          // overlapping (malformed) offsets overflow the output
-    if (d + m > NT) m = NT - d;
-    for (int col = 0; col < n_cols; ++col) {
-        const char *in = (const char *)cols.in[col];
-        char *out = (char *)cols.out[col];
-        const bool vec = cols.vec[col] != 0;
-        switch (cols.elem[col]) {
-            case 1: copy_piece<1>(in, out, vec, d, s, m); break;
-            case 2: copy_piece<2>(in, out, vec, d, s, m); break;
-            case 4: copy_piece<4>(in, out, vec, d, s, m); break;
-            default: copy_piece<8>(in, out, vec, d, s, m); break;
+        __syncthreads();
+        const int64_t d = piece[0], s = piece[1];
+        int64_t m = piece[2];
+        if (d >= NT || m <= 0) continue;        // overlapping (malformed) offsets overflow the output
+        if (d + m > NT) m = NT - d;
+        for (int col = 0; col < n_cols; ++col) {
+            const char *in = (const char *)cols.in[col];
+            char *out = (char *)cols.out[col];
+            const bool vec = cols.vec[col] != 0;
+            switch (cols.elem[col]) {
+                case 1: copy_piece<1>(in, out, vec, d, s, m); break;
+                case 2: copy_piece<2>(in, out, vec, d, s, m); break;
+                case 4: copy_piece<4>(in, out, vec, d, s, m); break;
+                default: copy_piece<8>(in, out, vec, d, s, m); break;
+            }
         }
     }
 }
@@ -487,11 +497,19 @@ hipError_t launch_compact_partials(const int64_t *offsets, int64_t n, int64_t n_
 hipError_t launch_compact_pieces(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                                  const PieceParts &parts, const CompactCols &cols, int n_cols,
                                  int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
-                                 int32_t *reject_ids, int64_t budget, hipStream_t stream) {
-    // Block workgroups, then at most n + n_tokens / kPieceLen piece workgroups
-    // (a span of len tokens has at most len / kPieceLen + 1 pieces).
+                                 int32_t *reject_ids, int64_t budget, int64_t max_kept,
+                                 hipStream_t stream) {
+    // Block workgroups, then the piece workgroups: a kept span of len tokens
+    // has at most len / kPieceLen + 1 pieces, so all kept spans together have
+    // at most max_kept + n_tokens / kPieceLen.
+    // Past one resident round of workgroups (8 per CU) the piece workgroups
+    // loop over the pieces instead.
     const int64_t nb = piece_blocks(n);
-    const int64_t grid = (nb > 0 ? nb : 1) + n + n_tokens / kPieceLen + 1;
+    const int64_t kept_bound = max_kept < 0 ? 0 : (max_kept > n ? n : max_kept);
+    int64_t piece_wgs = kept_bound + n_tokens / kPieceLen + 1;
+    const int64_t round = resident_waves() / 16 * 8 - nb;
+    if (round > 0 && piece_wgs > round) piece_wgs = round;
+    const int64_t grid = (nb > 0 ? nb : 1) + piece_wgs;
     return launch(kPhaseCompact, compact_piece_kernel, dim3((unsigned)grid), dim3(kPT), stream, offsets, n,
                   n_tokens, keep, parts, nb, cols, n_cols, offsets_out, kept_ids, n_kept_tokens,
                   reject_ids, budget);
@@ -517,7 +535,7 @@ hipError_t launch_compact(const int64_t *offsets, int64_t n, int64_t n_tokens, c
         hipError_t e = launch_compact_partials(offsets, n, n_tokens, keep, w.parts, stream);
         if (e != hipSuccess) return e;
         return launch_compact_pieces(offsets, n, n_tokens, keep, w.parts, cols, n_cols, offsets_out,
-                                     kept_ids, n_kept_tokens, nullptr, 0, stream);
+                                     kept_ids, n_kept_tokens, nullptr, 0, n, stream);
     }
     compact_scan_kernel<<<1, kT, 0, stream>>>(offsets, n, n_tokens, keep, offsets_out, kept_ids,
                                              n_kept_tokens, w.kept_src, w.chunk_first,

@@ -48,8 +48,10 @@ hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64
         const CompactWs cw = compact_ws_carve(cws_base, n, n_tokens);
         e = launch_rank(score, n, budget, keep, offsets, n_tokens, cw.parts, stream);
         if (e != hipSuccess) return e;
+        // The rank rejects exactly min(budget, n) trajectories.
+        const int64_t n_kept = n - (budget < n ? budget : n);
         return launch_compact_pieces(offsets, n, n_tokens, keep, cw.parts, cols, n_cols, offsets_out,
-                                     kept_ids, n_kept_tokens, reject_ids, budget, stream);
+                                     kept_ids, n_kept_tokens, reject_ids, budget, n_kept, stream);
     }
     e = launch_select(score, n, budget, keep, reject_ids, sel_ws, stream);
     if (e != hipSuccess) return e;

@@ -143,13 +143,16 @@ hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_to
 // workgroup per piece copies it. reject_ids may be NULL; when given, the ids
 // with keep == 0 go there in ascending order (at most `budget` of them).
 // The block partials come from the rank kernel or from launch_compact_partials.
+// max_kept bounds the number of kept trajectories (n when unknown); the grid
+// holds max_kept + n_tokens / kPieceLen piece workgroups.
 bool compact_piece_ok(int64_t n, int64_t n_tokens);
 hipError_t launch_compact_partials(const int64_t *offsets, int64_t n, int64_t n_tokens,
                                    const uint8_t *keep, const PieceParts &parts, hipStream_t stream);
 hipError_t launch_compact_pieces(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                                  const PieceParts &parts, const CompactCols &cols, int n_cols,
                                  int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
-                                 int32_t *reject_ids, int64_t budget, hipStream_t stream);
+                                 int32_t *reject_ids, int64_t budget, int64_t max_kept,
+                                 hipStream_t stream);
 hipError_t launch_compact(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                           const CompactCols &cols, int n_cols, int64_t *offsets_out,
                           int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, hipStream_t stream);

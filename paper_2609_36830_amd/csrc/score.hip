@@ -10,7 +10,8 @@
 // walks the trajectory boundaries that fall inside its chunk and keeps, per
 // lane, the running piece sum of (tag + 1) over generated tokens (masked
 // tags, -1, add 0) and the generated-token count. When a trajectory ends the
-// wave reduces the piece across lanes and lane 0 stores it:
+// wave reduces the piece across lanes and holds it in a lane until the chunk
+// is done, then stores every held piece at once:
 //   - the piece of a trajectory that starts inside this chunk goes to
 //     part_{sum,cnt}[trajectory] (exactly one chunk holds each start);
 //   - the piece of the trajectory that straddles the chunk start goes to
@@ -33,7 +34,7 @@ namespace {
 
 constexpr int kVec = 4;                       // tags per lane per window
 constexpr int kWin = kWave * kVec;            // 256 tokens per wave window
-constexpr int kUnroll = 4;                    // windows per super-window
+constexpr int kUnroll = 8;                    // windows per super-window
 constexpr int kSub = 4;                       // windows per fast-path / walk block
 constexpr bool kDoubleBuffer = false;         // two super-windows in flight
 constexpr int kWavesPerBlock = 4;
@@ -172,17 +173,35 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
     uint64_t acc_s = 0;
     uint32_t acc_c = 0;
 
+    // Finished pieces wait in registers, the k-th in lane k, and are stored
+    // after the last super-window: a store in mid-stream would hold up the
+    // next loads (the vector memory counter covers stores too). Past 64
+    // pieces a chunk stores directly.
+    int n_held = 0;                     // wave-uniform
+    uint64_t held_s = 0;
+    int64_t held_c = 0, held_at = 0;    // held_at: trajectory, or -1 for the carry
+    auto store_piece = [&](int64_t at, uint64_t ts, int64_t tc) {
+        if (at < 0) {
+            carry_sum[chunk] = ts;
+            carry_cnt[chunk] = tc;
+        } else {
+            part_sum[at] = ts;
+            part_cnt[at] = tc;
+        }
+    };
     auto flush = [&]() {
         const uint64_t ts = wave_sum_u64(acc_s);
-        const uint64_t tc = wave_sum_u64((uint64_t)acc_c);
-        if (lane == 0) {
-            if (carry_piece) {
-                carry_sum[chunk] = ts;
-                carry_cnt[chunk] = (int64_t)tc;
-            } else {
-                part_sum[cur] = ts;
-                part_cnt[cur] = (int64_t)tc;
+        const int64_t tc = (int64_t)wave_sum_u64((uint64_t)acc_c);
+        const int64_t at = carry_piece ? -1 : cur;
+        if (n_held < kWave) {
+            if (lane == n_held) {
+                held_s = ts;
+                held_c = tc;
+                held_at = at;
             }
+            ++n_held;
+        } else if (lane == 0) {
+            store_piece(at, ts, tc);
         }
         acc_s = 0;
         acc_c = 0;
@@ -273,6 +292,7 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
         }
     }
     if (pending) flush();
+    if (lane < n_held) store_piece(held_at, held_s, held_c);
 }
 
 template <bool kWinLds>

@@ -194,76 +194,105 @@ __global__ __launch_bounds__(kT) void select_reg_kernel(const double *__restrict
 // ---- rank by counting (pools of up to kRankMaxN trajectories) -------------
 // rank_i = #{j : key_j > key_i} + #{j < i : key_j == key_i} is the position of
 // trajectory i in the order (score desc, id asc); it is rejected iff
-// rank_i < budget. Every workgroup (1024 threads, 16 waves per CU so LDS
-// latency hides behind other waves) stages the keys in LDS, tile by tile,
-// and ranks kRankQ trajectories with kRankS threads each; a thread counts
-// over every kRankS-th key of the tile. The n^2 comparisons spread over the
-// whole device with no dependent rounds.
+// rank_i < budget. Every workgroup (1024 threads) ranks the kRankQ
+// trajectories of one block. A thread holds kKeys keys (j = t, t + 1024, ...)
+// in registers and tests each against all kRankQ targets, whose keys every
+// lane reads alike. The order on (key, id) is the unsigned order on the
+// 96-bit words (key, 2^32 - 1 - id): one three-word borrow chain per pair,
+// whose final borrow is the count increment. No LDS traffic per pair; the n^2
+// comparisons spread over the whole device with no dependent rounds.
 constexpr int kRankT = 1024;
 constexpr int kRankQ = 16;
-constexpr int kRankS = kRankT / kRankQ;
-constexpr int kRankTile = 4096;
+constexpr int kRankMaxKeys = (int)((kRankMaxN + kRankT - 1) / kRankT);
 
 static_assert(kRankQ == kPieceBlock, "a rank workgroup covers one partials block");
 
+struct RankKey {
+    uint32_t lo, hi, id;   // key bits 0..31, 32..63 and 2^32 - 1 - id
+};
+
+__device__ __forceinline__ RankKey rank_key(double s, int64_t j) {
+    const uint64_t k = score_key(s);
+    return RankKey{(uint32_t)k, (uint32_t)(k >> 32), ~(uint32_t)j};
+}
+
+// c + 1 if (key, id) of b precedes that of a in the order (score desc, id
+// asc), else c: the borrow out of a - b over the three words, added to c.
+// Written as the carry chain itself (the compiler expands the equivalent C
+// into compares and mask logic, four times the instructions). Each VALU that
+// reads the carry a previous VALU wrote is two wait states behind it.
+__device__ __forceinline__ uint32_t rank_add_beats(uint32_t c, const RankKey &a, const RankKey &b) {
+    uint32_t d;
+    asm("v_sub_co_u32_e32 %1, vcc, %2, %5\n\t"
+        "s_nop 1\n\t"
+        "v_subb_co_u32_e32 %1, vcc, %3, %6, vcc\n\t"
+        "s_nop 1\n\t"
+        "v_subb_co_u32_e32 %1, vcc, %4, %7, vcc\n\t"
+        "s_nop 1\n\t"
+        "v_addc_co_u32_e32 %0, vcc, 0, %0, vcc"
+        : "+v"(c), "=&v"(d)
+        : "v"(a.id), "v"(a.lo), "v"(a.hi), "v"(b.id), "v"(b.lo), "v"(b.hi)
+        : "vcc");
+    return c;
+}
+
+template <int kKeys>
 __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__ score, int64_t n,
                                                      int64_t budget, uint8_t *__restrict__ keep,
                                                      const int64_t *__restrict__ off, int64_t NT,
                                                      PieceParts parts) {
-    __shared__ uint64_t tile[kRankTile];
-    __shared__ uint32_t part[kRankT / kWave][kRankQ + 1];
+    __shared__ uint32_t part[kRankT / kWave][kRankQ];
     const int t = threadIdx.x;
-    const int q = t % kRankQ, s = t / kRankQ;
-    const int32_t i = (int32_t)((int64_t)blockIdx.x * kRankQ + q);
-    const uint64_t ki = score_key(i < n ? score[i] : 0.0);
-    // Span length of this workgroup's trajectories, for the block partials.
+    const int64_t i0 = (int64_t)blockIdx.x * kRankQ;
+    // All loads first: this thread's keys, the targets, the block's spans.
+    double v[kKeys];
+#pragma unroll
+    for (int u = 0; u < kKeys; ++u) {
+        const int64_t j = t + (int64_t)u * kRankT;
+        v[u] = j < n ? score[j] : 0.0;
+    }
+    double vq[kRankQ];
+#pragma unroll
+    for (int q = 0; q < kRankQ; ++q) vq[q] = i0 + q < n ? score[i0 + q] : 0.0;
     int64_t span = 0;
-    if (parts.cnt && t < kRankQ && i < n) {
-        const int64_t lo = clamp64(off[i], 0, NT), hi = clamp64(off[i + 1], 0, NT);
+    if (parts.cnt && t < kRankQ && i0 + t < n) {
+        const int64_t lo = clamp64(off[i0 + t], 0, NT), hi = clamp64(off[i0 + t + 1], 0, NT);
         span = hi > lo ? hi - lo : 0;
     }
-    uint32_t cnt = 0;
-    for (int64_t b0 = 0; b0 < n; b0 += kRankTile) {
-        const int m = (int)((n - b0) < kRankTile ? (n - b0) : kRankTile);
-        __syncthreads();
-        // all of a thread's loads in flight at once, then the keys
-        constexpr int kPer = kRankTile / kRankT;
-        double v[kPer];
+    // Padding keys are (0, 0, 0): below every target, so they never count.
+    RankKey kj[kKeys];
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int x = t + u * kRankT;
-            v[u] = x < m ? score[b0 + x] : 0.0;
-        }
+    for (int u = 0; u < kKeys; ++u) {
+        const int64_t j = t + (int64_t)u * kRankT;
+        kj[u] = j < n ? rank_key(v[u], j) : RankKey{0u, 0u, 0u};
+    }
+    uint32_t cnt[kRankQ];
 #pragma unroll
-        for (int u = 0; u < kPer; ++u) {
-            const int x = t + u * kRankT;
-            if (x < m) tile[x] = score_key(v[u]);
-        }
-        __syncthreads();
-        const int32_t jb = (int32_t)b0;
-        int x = s;
-        for (; x + 7 * kRankS < m; x += 8 * kRankS) {
-            uint64_t kj[8];
+    for (int q = 0; q < kRankQ; ++q) {
+        const RankKey kq = rank_key(vq[q], i0 + q);
+        uint32_t c = 0;
 #pragma unroll
-            for (int u = 0; u < 8; ++u) kj[u] = tile[x + u * kRankS];
+        for (int u = 0; u < kKeys; ++u) c = rank_add_beats(c, kq, kj[u]);
+        cnt[q] = c;
+    }
+    // Wave sums, three counts to a word (a wave adds at most 64 * kKeys <= 512
+    // per target: 10 bits), then the 16 waves' sums through LDS.
+    static_assert(kWave * kRankMaxKeys < 1024, "packed wave counts fit 10 bits");
 #pragma unroll
-            for (int u = 0; u < 8; ++u)
-                cnt += (kj[u] > ki || (kj[u] == ki && jb + x + u * kRankS < i)) ? 1u : 0u;
-        }
-        for (; x < m; x += kRankS) {
-            const uint64_t kj = tile[x];
-            cnt += (kj > ki || (kj == ki && jb + x < i)) ? 1u : 0u;
+    for (int q0 = 0; q0 < kRankQ; q0 += 3) {
+        uint32_t w = cnt[q0];
+        if (q0 + 1 < kRankQ) w |= cnt[q0 + 1] << 10;
+        if (q0 + 2 < kRankQ) w |= cnt[q0 + 2] << 20;
+        w = wave_incl_scan_u32(w);
+        if (lane_id() == kWave - 1) {
+            part[t / kWave][q0] = w & 1023u;
+            if (q0 + 1 < kRankQ) part[t / kWave][q0 + 1] = (w >> 10) & 1023u;
+            if (q0 + 2 < kRankQ) part[t / kWave][q0 + 2] = w >> 20;
         }
     }
-    // A wave holds four slices of every target (lane = slice * 16 + target):
-    // add them with two butterflies, then the 16 waves' sums through LDS.
-    static_assert(kRankQ * 4 == kWave, "four slices per wave");
-    cnt += (uint32_t)__shfl_xor((int)cnt, kRankQ, kWave);
-    cnt += (uint32_t)__shfl_xor((int)cnt, 2 * kRankQ, kWave);
-    if ((t % kWave) < kRankQ) part[t / kWave][q] = cnt;
     __syncthreads();
     if (t < kWave) {   // wave 0; lanes below kRankQ own the targets
-        const int64_t ii = (int64_t)blockIdx.x * kRankQ + t;
+        const int64_t ii = i0 + t;
         bool kept = false;
         if (t < kRankQ && ii < n) {
             uint32_t r = 0;
@@ -320,8 +349,16 @@ hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *
                        const int64_t *offsets, int64_t n_tokens, const PieceParts &parts,
                        hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    return launch(kPhaseSelect, rank_kernel, dim3((unsigned)((n + kRankQ - 1) / kRankQ)), dim3(kRankT),
-                  stream, score, n, budget, keep, offsets, n_tokens, parts);
+    if (n > kRankMaxN) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((n + kRankQ - 1) / kRankQ));
+#define PACE_RANK(K) \
+    return launch(kPhaseSelect, rank_kernel<K>, grid, dim3(kRankT), stream, score, n, budget, keep, offsets, \
+                  n_tokens, parts)
+    if (n <= kRankT) PACE_RANK(1);
+    if (n <= 2 * kRankT) PACE_RANK(2);
+    if (n <= 4 * kRankT) PACE_RANK(4);
+    PACE_RANK(8);
+#undef PACE_RANK
 }
 
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
