@@ -196,14 +196,18 @@ __device__ __forceinline__ void copy_range_col(const CompactCols &cols, int col,
 constexpr int kPT = 256;                  // threads of a piece workgroup
 constexpr int kPW = kPT / kWave;          // its waves
 constexpr int kPartsPerThread = (int)((kPieceMaxN / kPieceBlock + kPT - 1) / kPT);
+constexpr int kCopyU = 4;                 // 16-byte loads in flight per thread in a piece copy
 
 // Span length of trajectory i if kept (offsets clamped to [0, NT]), else 0.
+// (The flag and both offsets are loaded together: one round trip.)
 __device__ __forceinline__ int64_t kept_span(const int64_t *__restrict__ off, const uint8_t *__restrict__ keep,
                                              int64_t i, int64_t NT, int64_t &lo) {
+    const bool k = keep[i] != 0;
+    const int64_t a = off[i], b = off[i + 1];
     lo = 0;
-    if (keep[i] == 0) return -1;
-    lo = clamp64(off[i], 0, NT);
-    const int64_t hi = clamp64(off[i + 1], 0, NT);
+    if (!k) return -1;
+    lo = clamp64(a, 0, NT);
+    const int64_t hi = clamp64(b, 0, NT);
     return hi > lo ? hi - lo : 0;
 }
 
@@ -246,8 +250,17 @@ __device__ __forceinline__ void copy_piece(const char *__restrict__ in, char *__
         if (a0 < a1) {
             if (t < a0 - d) dst[d + t] = src[d + t + delta];
             if (t < e - a1) dst[a1 + t] = src[a1 + t + delta];
-            for (int64_t v = a0 / VE + t; v < a1 / VE; v += kPT)
-                store_nt(reinterpret_cast<uint4 *>(dst + v * VE), load_a4(src + v * VE + delta));
+            // kCopyU loads in flight per thread, then their stores.
+            const int64_t v1 = a1 / VE;
+            int64_t v = a0 / VE + t;
+            for (; v + (kCopyU - 1) * kPT < v1; v += kCopyU * kPT) {
+                uint4 x[kCopyU];
+#pragma unroll
+                for (int u = 0; u < kCopyU; ++u) x[u] = load_a4(src + (v + u * kPT) * VE + delta);
+#pragma unroll
+                for (int u = 0; u < kCopyU; ++u) store_nt(reinterpret_cast<uint4 *>(dst + (v + u * kPT) * VE), x[u]);
+            }
+            for (; v < v1; v += kPT) store_nt(reinterpret_cast<uint4 *>(dst + v * VE), load_a4(src + v * VE + delta));
             return;
         }
     }

@@ -295,13 +295,18 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
     if (lane < n_held) store_piece(held_at, held_s, held_c);
 }
 
+// Finalize workgroup size: small, so the few thousand trajectories of a pool
+// spread over many CUs.
+constexpr int kFinT = 128;
+
 template <bool kWinLds>
-__global__ __launch_bounds__(256) void score_finalize_kernel(
+__global__ __launch_bounds__(kFinT) void score_finalize_kernel(
     const int64_t *__restrict__ off, int64_t n, int64_t NT, const int32_t *__restrict__ completion,
     int32_t V, const double *__restrict__ prefix, const double *__restrict__ window, int64_t W,
     int use_prefix, double w_wait, int gamma, int64_t chunk_len, ScoreWorkspace ws,
     double *__restrict__ score, int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count) {
     __shared__ double win_lds[kWinLds ? kWindowLdsMax : 1];
+    const bool narrow = (NT >> 11) < ((int64_t)1 << 32);   // token positions below 2^43
     // The trajectory's own loads go first (they do not wait for the window),
     // then the window is staged; every thread reaches the barrier.
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -316,11 +321,12 @@ __global__ __launch_bounds__(256) void score_finalize_kernel(
         if (use_prefix) s_pre = prefix[i];
     }
     const TrajPieces pc = in ? gather_pieces(i, lo, hi, ws.part_sum, ws.part_cnt, ws.carry_sum, ws.carry_cnt,
-                                             chunk_len)
+                                             chunk_len, narrow)
                              : TrajPieces{0, 0};
     if (kWinLds && use_prefix) {
+        const int w_n = (int)W;                  // W <= kWindowLdsMax here
 #pragma unroll 4
-        for (int64_t k = threadIdx.x; k < W; k += blockDim.x) win_lds[k] = window[k];
+        for (int k = (int)threadIdx.x; k < w_n; k += kFinT) win_lds[k] = window[k];
         __syncthreads();
     }
     if (!in) return;
@@ -377,12 +383,12 @@ hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_to
                                  int gamma, int64_t chunk_len, double *score, int64_t *gen_sum,
                                  int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    const unsigned grid = (unsigned)((n + 255) / 256);
+    const unsigned grid = (unsigned)((n + kFinT - 1) / kFinT);
     if (use_prefix && W <= kWindowLdsMax)
-        return launch(kPhaseFinalize, score_finalize_kernel<true>, dim3(grid), dim3(256), stream, offsets,
+        return launch(kPhaseFinalize, score_finalize_kernel<true>, dim3(grid), dim3(kFinT), stream, offsets,
                       n, n_tokens, completion, V, prefix, window, W, 1, w_wait, gamma, chunk_len, ws,
                       score, gen_sum, gen_count);
-    return launch(kPhaseFinalize, score_finalize_kernel<false>, dim3(grid), dim3(256), stream, offsets, n,
+    return launch(kPhaseFinalize, score_finalize_kernel<false>, dim3(grid), dim3(kFinT), stream, offsets, n,
                   n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma,
                   chunk_len, ws, score, gen_sum, gen_count);
 }

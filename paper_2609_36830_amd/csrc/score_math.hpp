@@ -1,5 +1,5 @@
-// Per-trajectory score of the PACE filter (Sec. 2, Sec. 3.2), shared by the
-// finalize kernel and the fused filter-step kernel.
+// Per-trajectory score of the PACE filter (Sec. 2, Sec. 3.2), as the
+// finalize kernel forms it from the reduction's pieces.
 //
 //   T      generated (tag != -1) tokens                        Eq. (1)
 //   S      sum over them of (c - tag) = c T - sum(tag), exact   Eq. (2)
@@ -29,16 +29,43 @@ struct TrajPieces {
     int64_t T;     // generated tokens
 };
 
-// Pieces of trajectory i covering tokens [lo, hi).
+// Chunk holding token position p >= 0. The chunk length is a multiple of
+// kScoreChunkAlign = 2^11, so p / chunk_len = (p >> 11) / (chunk_len >> 11);
+// with narrow (every position below 2^43) that is a 32-bit division.
+__device__ __forceinline__ int64_t chunk_of(int64_t p, int64_t chunk_len, bool narrow) {
+    static_assert(kScoreChunkAlign == 2048, "chunk lengths are multiples of 2^11");
+    if (narrow) return (int64_t)((uint32_t)(p >> 11) / (uint32_t)(chunk_len >> 11));
+    return p / chunk_len;
+}
+
+// Pieces of trajectory i covering tokens [lo, hi): its part and the carries
+// of chunks lo / chunk_len + 1 .. (hi - 1) / chunk_len. The first kCarryBatch
+// carries are loaded together (one round trip); longer spans loop.
+constexpr int kCarryBatch = 4;
 __device__ __forceinline__ TrajPieces gather_pieces(
     int64_t i, int64_t lo, int64_t hi, const uint64_t *__restrict__ part_sum,
     const int64_t *__restrict__ part_cnt, const uint64_t *__restrict__ carry_sum,
-    const int64_t *__restrict__ carry_cnt, int64_t chunk_len) {
+    const int64_t *__restrict__ carry_cnt, int64_t chunk_len, bool narrow) {
     TrajPieces p{0, 0};
     if (hi > lo) {
         p.sp = part_sum[i];
         p.T = part_cnt[i];
-        for (int64_t ch = lo / chunk_len + 1; ch * chunk_len < hi; ++ch) {
+        const int64_t first = chunk_of(lo, chunk_len, narrow) + 1;
+        const int64_t last = chunk_of(hi - 1, chunk_len, narrow);
+        uint64_t cs[kCarryBatch];
+        int64_t cc[kCarryBatch];
+#pragma unroll
+        for (int u = 0; u < kCarryBatch; ++u) {
+            const bool in = first + u <= last;
+            cs[u] = in ? carry_sum[first + u] : 0;
+            cc[u] = in ? carry_cnt[first + u] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kCarryBatch; ++u) {
+            p.sp += cs[u];
+            p.T += cc[u];
+        }
+        for (int64_t ch = first + kCarryBatch; ch <= last; ++ch) {
             p.sp += carry_sum[ch];
             p.T += carry_cnt[ch];
         }

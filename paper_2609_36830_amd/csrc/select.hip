@@ -197,10 +197,12 @@ __global__ __launch_bounds__(kT) void select_reg_kernel(const double *__restrict
 // rank_i < budget. Every workgroup (1024 threads) ranks the kRankQ
 // trajectories of one block. A thread holds kKeys keys (j = t, t + 1024, ...)
 // in registers and tests each against all kRankQ targets, whose keys every
-// lane reads alike. The order on (key, id) is the unsigned order on the
-// 96-bit words (key, 2^32 - 1 - id): one three-word borrow chain per pair,
-// whose final borrow is the count increment. No LDS traffic per pair; the n^2
-// comparisons spread over the whole device with no dependent rounds.
+// lane reads alike. Where all ids of a wave's key slot lie below (above) the
+// targets' ids, the id tie-break is a fixed direction and one 64-bit compare
+// decides; in the one slot that shares the targets' group, (key, id) is
+// compared as the 96-bit word (key, 2^32 - 1 - id) by a borrow chain. No LDS
+// traffic per pair; the n^2 comparisons spread over the whole device with no
+// dependent rounds.
 constexpr int kRankT = 1024;
 constexpr int kRankQ = 16;
 constexpr int kRankMaxKeys = (int)((kRankMaxN + kRankT - 1) / kRankT);
@@ -210,11 +212,6 @@ static_assert(kRankQ == kPieceBlock, "a rank workgroup covers one partials block
 struct RankKey {
     uint32_t lo, hi, id;   // key bits 0..31, 32..63 and 2^32 - 1 - id
 };
-
-__device__ __forceinline__ RankKey rank_key(double s, int64_t j) {
-    const uint64_t k = score_key(s);
-    return RankKey{(uint32_t)k, (uint32_t)(k >> 32), ~(uint32_t)j};
-}
 
 // c + 1 if (key, id) of b precedes that of a in the order (score desc, id
 // asc), else c: the borrow out of a - b over the three words, added to c.
@@ -251,29 +248,60 @@ __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__
         const int64_t j = t + (int64_t)u * kRankT;
         v[u] = j < n ? score[j] : 0.0;
     }
-    double vq[kRankQ];
-#pragma unroll
-    for (int q = 0; q < kRankQ; ++q) vq[q] = i0 + q < n ? score[i0 + q] : 0.0;
+    // Lane q of every wave loads target q; its key is formed in the vector
+    // unit and read out to scalars (a scalar-side conversion branches on
+    // every target).
+    const int lane = lane_id();
+    const double vq = lane < kRankQ && i0 + lane < n ? score[i0 + lane] : 0.0;
     int64_t span = 0;
     if (parts.cnt && t < kRankQ && i0 + t < n) {
         const int64_t lo = clamp64(off[i0 + t], 0, NT), hi = clamp64(off[i0 + t + 1], 0, NT);
         span = hi > lo ? hi - lo : 0;
     }
-    // Padding keys are (0, 0, 0): below every target, so they never count.
-    RankKey kj[kKeys];
+    // Padding keys are 0: below every target key (the smallest key of a
+    // number is that of -inf, above 0), so they never count.
+    uint64_t kj[kKeys];
 #pragma unroll
     for (int u = 0; u < kKeys; ++u) {
         const int64_t j = t + (int64_t)u * kRankT;
-        kj[u] = j < n ? rank_key(v[u], j) : RankKey{0u, 0u, 0u};
+        kj[u] = j < n ? score_key(v[u]) : 0ull;
     }
-    uint32_t cnt[kRankQ];
+    const uint64_t kq_lane = score_key(vq);
+    uint64_t kq[kRankQ], kq_m1[kRankQ];
 #pragma unroll
     for (int q = 0; q < kRankQ; ++q) {
-        const RankKey kq = rank_key(vq[q], i0 + q);
-        uint32_t c = 0;
+        kq[q] = (uint64_t)readlane_i64((int64_t)kq_lane, q);
+        kq_m1[q] = kq[q] - 1;
+    }
+    // Key slot u of this wave holds ids [64 g, 64 g + 64), g = wave + 16 u;
+    // the targets all lie in group i0 / 64. For a slot in a lower group every
+    // id is below every target's, so j beats q iff key_j >= key_q, that is
+    // key_j > key_q - 1; in a higher group iff key_j > key_q. Only the slot
+    // of the targets' own group compares (key, id) in full.
+    const int64_t g_t = i0 / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(t / kWave);   // uniform: keeps the tests scalar
+    uint32_t cnt[kRankQ];
 #pragma unroll
-        for (int u = 0; u < kKeys; ++u) c = rank_add_beats(c, kq, kj[u]);
-        cnt[q] = c;
+    for (int q = 0; q < kRankQ; ++q) cnt[q] = 0;
+#pragma unroll
+    for (int u = 0; u < kKeys; ++u) {
+        const int64_t g = wave + (int64_t)u * (kRankT / kWave);
+        if (g < g_t) {
+#pragma unroll
+            for (int q = 0; q < kRankQ; ++q) cnt[q] += kj[u] > kq_m1[q] ? 1u : 0u;
+        } else if (g > g_t) {
+#pragma unroll
+            for (int q = 0; q < kRankQ; ++q) cnt[q] += kj[u] > kq[q] ? 1u : 0u;
+        } else {
+            const int64_t j = t + (int64_t)u * kRankT;
+            const RankKey b = j < n ? RankKey{(uint32_t)kj[u], (uint32_t)(kj[u] >> 32), ~(uint32_t)j}
+                                    : RankKey{0u, 0u, 0u};
+#pragma unroll
+            for (int q = 0; q < kRankQ; ++q) {
+                const RankKey a{(uint32_t)kq[q], (uint32_t)(kq[q] >> 32), ~(uint32_t)(i0 + q)};
+                cnt[q] = rank_add_beats(cnt[q], a, b);
+            }
+        }
     }
     // Wave sums, three counts to a word (a wave adds at most 64 * kKeys <= 512
     // per target: 10 bits), then the 16 waves' sums through LDS.
