@@ -82,8 +82,8 @@ def reduce_traffic(config):
 
 # config -> {"sha256": digest of the score_reduce sources, "bytes": HBM bytes per launch}
 REDUCE_COUNTERS = {
-    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98114.2 KiB, WRITE_SIZE 264.5 KiB
-    "stress": {"sha256": "773337b866379c7e6d732d0d3ffbe61dccd6da6e9a28f12577342305480fe729", "bytes": 201208730},
+    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98154.6 KiB, WRITE_SIZE 175.8 KiB
+    "stress": {"sha256": "5cd1a9811c0657887464ebfa0b38324bdcffef4ce3796c42577416e98f8f3a68", "bytes": 201200707},
 }
 
 
