@@ -405,12 +405,13 @@ def main():
     gws = torch.empty(pace.pace_workspace_bytes(pace.WS_FILTER_STEP, max(pool.n, n_groups), pool.n_tokens),
                       dtype=torch.uint8, device=dev)
     gev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(K + 2)]
+    gout = pace.group_step_buffers(pool.n, n_groups, cols, dev)
     g_res = None
     for k in range(K + 2):
         flush.max()
         gev[k][0].record(stream)
         g_res = pace.pace_group_filter_step(tags, off, comp, pool.V, go, g_occ, g_cap, cols, prefix, window,
-                                            params, 0.0, workspace=gws)
+                                            params, 0.0, workspace=gws, out=gout)
         gev[k][1].record(stream)
     torch.cuda.synchronize()
     g_ms = np.array([e[0].elapsed_time(e[1]) for e in gev[2:]])

@@ -292,12 +292,26 @@ def pace_validate_groups(group_offsets, n_traj: int, err_out=None, stream=None):
     return err_out
 
 
+def group_step_buffers(n: int, n_groups: int, cols, device):
+    """Output buffers for repeated pace_group_filter_step calls on pools of at
+    most n trajectories, n_groups groups and the columns' sizes (pass as
+    ``out``): no allocation inside the calls."""
+    e = lambda k, dt: torch.empty(k, dtype=dt, device=device)
+    return dict(score=e(max(n, 1), torch.float64), gen_sum=e(max(n, 1), torch.int64),
+                gen_count=e(max(n, 1), torch.int64), group_score=e(max(n_groups, 1), torch.float64),
+                group_keep=e(max(n_groups, 1), torch.uint8), reject_group_ids=e(max(n_groups, 1), torch.int32),
+                keep=e(max(n, 1), torch.uint8), cols_out=[torch.empty_like(c) for c in cols],
+                offsets_out=e(n + 1, torch.int64), kept_ids=e(max(n, 1), torch.int32),
+                n_kept_tokens=e(1, torch.int64))
+
+
 def pace_group_filter_step(tags, offsets, completion, current_version, group_offsets, occupancy, capacity,
                            cols, prefix_score=None, window_sorted=None, params: Optional[PaceParams] = None,
-                           r_hat_prev: float = 0.0, workspace=None, stream=None):
+                           r_hat_prev: float = 0.0, workspace=None, stream=None, out=None):
     """One filter step with prompt groups as the admission unit (occupancy and
     capacity count groups). Returns a dict like pace_filter_step plus
-    group_score, group_keep and reject_group_ids (cut to the budget)."""
+    group_score, group_keep and reject_group_ids (cut to the budget). ``out``:
+    buffers from group_step_buffers, written in place of fresh ones."""
     _dev(tags, torch.int32, "tags")
     _dev(offsets, torch.int64, "offsets")
     _dev(completion, torch.int32, "completion")
@@ -316,14 +330,19 @@ def pace_group_filter_step(tags, offsets, completion, current_version, group_off
     for k, c in enumerate(cols):
         if not c.is_cuda or not c.is_contiguous() or c.numel() != nt:
             raise ValueError("column %d must be a contiguous device tensor of n_tokens elements" % k)
-    e = lambda k, dt: torch.empty(k, dtype=dt, device=dev)
-    score_out, gen_sum_out, gen_count_out = e(n, torch.float64), e(n, torch.int64), e(n, torch.int64)
-    group_score_out, group_keep_out = e(max(ng, 1), torch.float64), e(max(ng, 1), torch.uint8)
-    reject_group_ids_out = e(max(ng, 1), torch.int32)
-    keep_out = e(max(n, 1), torch.uint8)
-    cols_out = [torch.empty_like(c) for c in cols]
-    offsets_out, kept_ids_out = e(n + 1, torch.int64), e(max(n, 1), torch.int32)
-    n_kept_tokens_out = e(1, torch.int64)
+    o = out if out is not None else group_step_buffers(n, ng, cols, dev)
+    if (o["score"].numel() < max(n, 1) or o["group_score"].numel() < max(ng, 1)
+            or o["offsets_out"].numel() < n + 1 or len(o["cols_out"]) != len(cols)
+            or any(a.numel() < c.numel() or a.dtype != c.dtype or not a.is_contiguous()
+                   for a, c in zip(o["cols_out"], cols))):
+        raise ValueError("out buffers are too small for this pool, or do not match its columns")
+    score_out, gen_sum_out, gen_count_out = o["score"][:n], o["gen_sum"][:n], o["gen_count"][:n]
+    group_score_out, group_keep_out = o["group_score"], o["group_keep"]
+    reject_group_ids_out = o["reject_group_ids"]
+    keep_out = o["keep"]
+    cols_out = [a[:nt] for a in o["cols_out"]]
+    offsets_out, kept_ids_out = o["offsets_out"][: n + 1], o["kept_ids"]
+    n_kept_tokens_out = o["n_kept_tokens"]
     ws = _workspace(WS_FILTER_STEP, max(n, ng), nt, dev, workspace)
     nc = len(cols)
     cin = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols])

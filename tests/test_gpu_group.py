@@ -53,13 +53,13 @@ def random_groups(rng, n, max_size=12, empty_frac=0.1, trailing_empty=True):
     return np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
 
 
-def group_step_parity(pace, pool, go, occ, cap, mode="effective"):
+def group_step_parity(pace, pool, go, occ, cap, mode="effective", out=None):
     params = pace.default_params(w_wait=0.0 if mode == "gen" else 1.0)
     prefix = None if mode == "raw" else D(pool.prefix_score)
     window = None if mode == "raw" else D(pool.window)
     tags = D(pool.tags)
     r = pace.pace_group_filter_step(tags, D(pool.offsets), D(pool.completion), pool.V, D(go), occ, cap, [tags],
-                                    prefix, window, params)
+                                    prefix, window, params, out=out(tags) if out else None)
     torch.cuda.synchronize()
     o = oracle.group_filter_step(pool, go, occ, cap, mode=mode)
     assert r["budget"] == o["budget"]
@@ -103,6 +103,24 @@ def test_group_step_stress_pool(pace, grouping):
     ng = len(go) - 1
     say("group step stress pool grouping=%s groups=%d" % (grouping, ng))
     group_step_parity(pace, pool, go, ng, ng // 3)
+
+
+def test_group_step_reused_buffers(pace):
+    """Preallocated outputs, reused across calls on two different pools of the
+    same shape, give the oracle's results each time."""
+    pool_a = poolgen.make_pool("math", n=300)
+    pool_b = poolgen.make_pool("math", n=300, seed=9)
+    go = np.arange(0, pool_a.n + 1, 4, dtype=np.int64)
+    ng = len(go) - 1
+    big = pool_a if pool_a.n_tokens >= pool_b.n_tokens else pool_b
+    bufs = pace.group_step_buffers(pool_a.n, ng, [D(big.tags)], DEV)
+    say("group step reused buffers, %d groups, %d and %d tokens" % (ng, pool_a.n_tokens, pool_b.n_tokens))
+    for pool in (pool_a, pool_b, pool_a):
+        group_step_parity(pace, pool, go, ng, ng // 3, out=lambda tags: bufs)
+    with pytest.raises(ValueError):
+        t = D(big.tags)
+        pace.pace_group_filter_step(t, D(big.offsets), D(big.completion), big.V, D(go), ng, ng // 3,
+                                    [t], out=pace.group_step_buffers(big.n, ng, [t[:-1]], DEV))
 
 
 def test_group_step_more_groups_than_trajectories(pace):
