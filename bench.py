@@ -34,7 +34,7 @@ METRIC = "pool filter step: tokens/s and trajectories/s, % of HBM peak GB/s"
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", default="stress")
     ap.add_argument("--mode", default="effective", choices=["effective", "raw", "gen"])
@@ -51,6 +51,18 @@ def parse():
 
 # (timer phase, kernel) of the fused step's launches
 PHASES = ((0, "score_reduce"), (1, "score_finalize"), (2, "rank"), (3, "compact_piece"))
+
+
+def cpu_model():
+    """The host CPU's model name, from /proc/cpuinfo where there is one."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
 
 
 def reduce_bytes(pool, cus):
@@ -519,7 +531,8 @@ def main():
         out["cpu_baseline"] = {
             "value": reps * pool.n_tokens / t_cpu, "unit": "tokens/s", "cores": 1, "kind": "oracle",
             "sample": "%d full oracle filter steps (score, budget, select, compact) on the same "
-                      "%s pool, single-threaded C, %.1f s" % (reps, args.config, t_cpu),
+                      "%s pool, single-threaded C, %.1f s, on %s (%d host threads visible)"
+                      % (reps, args.config, t_cpu, cpu_model(), os.cpu_count() or 0),
         }
     print(json.dumps(out))
 
