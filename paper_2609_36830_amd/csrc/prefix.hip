@@ -4,16 +4,16 @@
 // NaN when fewer than `min_tokens` are eligible.
 //
 // One 256-thread workgroup per prefix, HBM-bound (8 bytes per token, 12 with
-// tags). A round covers 1024 tokens: each wave takes 256 of them as four rows
-// of 64 consecutive tokens, so every load instruction reads 256 contiguous
-// bytes, and all of a round's loads are in flight together (one round covers
-// a whole capped prefix unless many tokens are masked). A token's position in
-// the eligible order is the running count plus the eligible tokens of earlier
-// waves (LDS), earlier rows (ballot) and lower lanes in its row; tokens at
-// position >= cap are skipped and the walk stops once the cap is reached.
-// Each lane adds its terms in binary64; a butterfly of shuffles sums a wave,
-// and thread 0 adds the four wave sums in order (a fixed order, so results
-// repeat bit for bit).
+// tags). A round covers 1024 tokens, four consecutive ones per thread, read
+// as one 16-byte vector per array (dword-aligned loads; the prefix's last
+// partial vector element by element), all of a round's loads in flight
+// together (one round covers a whole capped prefix unless many tokens are
+// masked). A token's position in the eligible order is the running count plus
+// a block exclusive scan of the threads' eligible counts plus the eligible
+// tokens before it in its thread; tokens at position >= cap are skipped and
+// the walk stops once the cap is reached. Each lane adds its terms in
+// binary64; a butterfly of shuffles sums a wave, and thread 0 adds the four
+// wave sums in order (a fixed order, so results repeat bit for bit).
 #include "device_util.hpp"
 #include "kernels.hpp"
 
@@ -23,12 +23,26 @@ namespace pace {
 
 namespace {
 
-constexpr int kPRows = 4;
+constexpr int kPT4 = 4;   // tokens per thread per round
 
 __device__ __forceinline__ double wave_sum_f64(double v) {
 #pragma unroll
     for (int off = kWave / 2; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
     return v;
+}
+
+// Elements [p, p + 4) of a 4-byte array, those at or past hi as `fill`.
+template <typename T>
+__device__ __forceinline__ void load4(const T *__restrict__ a, int64_t p, int64_t hi, T fill, T (&v)[kPT4]) {
+    if (p + kPT4 <= hi) {
+        const uint4 x = load_a4(a + p);
+        const uint32_t w[kPT4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+        for (int e = 0; e < kPT4; ++e) v[e] = __builtin_bit_cast(T, w[e]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < kPT4; ++e) v[e] = p + e < hi ? a[p + e] : fill;
+    }
 }
 
 template <bool kTags>
@@ -39,56 +53,41 @@ __global__ __launch_bounds__(256) void prefix_score_kernel(const float *__restri
                                                           int64_t NT, int64_t cap, int64_t min_tokens,
                                                           double *__restrict__ out) {
     constexpr int kW = 256 / kWave;                   // waves per prefix
-    constexpr int64_t kSpan = (int64_t)256 * kPRows;  // tokens per round (1024)
-    __shared__ int64_t wcnt[kW];
+    constexpr int64_t kSpan = (int64_t)256 * kPT4;    // tokens per round (1024)
+    __shared__ uint32_t wsum[kW];
     __shared__ double wacc[kW];
     const int64_t i = blockIdx.x;
     if (i >= n) return;
     const int lane = lane_id();
     const int wave = threadIdx.x / kWave;
     const int64_t lo = clamp64(po[i], 0, NT), hi = clamp64(po[i + 1], 0, NT);
-    const uint64_t below = lanes_below();
     double acc = 0.0;
     int64_t m = 0;                                   // eligible tokens before the current round
     for (int64_t w = lo; w < hi && m < cap; w += kSpan) {
-        // this wave's 256 tokens, four rows of 64
-        const int64_t wb = w + (int64_t)wave * kWave * kPRows;
-        float a[kPRows], b[kPRows];
-        bool e[kPRows];
-        uint64_t bal[kPRows];
-        int64_t mine = 0;
+        const int64_t p = w + (int64_t)threadIdx.x * kPT4;
+        float a[kPT4], b[kPT4];
+        int32_t tg[kPT4];
+        load4<float>(lp_new, p, hi, 0.0f, a);
+        load4<float>(lp_beh, p, hi, 0.0f, b);
+        if (kTags) load4<int32_t>(tags, p, hi, -1, tg);
+        bool e[kPT4];
+        uint32_t cnt = 0;
 #pragma unroll
-        for (int k = 0; k < kPRows; ++k) {
-            const int64_t p = wb + (int64_t)k * kWave + lane;
-            const bool in = p < hi;
-            e[k] = in && (!kTags || tags[p] != -1);
-            a[k] = in ? lp_new[p] : 0.0f;
-            b[k] = in ? lp_beh[p] : 0.0f;
+        for (int k = 0; k < kPT4; ++k) {
+            e[k] = p + k < hi && (!kTags || tg[k] != -1);
+            cnt += e[k] ? 1u : 0u;
         }
+        uint32_t total;
+        const uint32_t before = block_excl_sum_u32<kW>(cnt, total, wsum);
+        int64_t idx = m + before;
 #pragma unroll
-        for (int k = 0; k < kPRows; ++k) {
-            bal[k] = ballot(e[k]);
-            mine += (int64_t)__popcll(bal[k]);
-        }
-        if (lane == 0) wcnt[wave] = mine;
-        __syncthreads();
-        int64_t row_base = m, total = m;
-#pragma unroll
-        for (int v = 0; v < kW; ++v) {
-            row_base += (v < wave) ? wcnt[v] : 0;
-            total += wcnt[v];
-        }
-#pragma unroll
-        for (int k = 0; k < kPRows; ++k) {
-            const int64_t idx = row_base + (int64_t)__popcll(bal[k] & below);
-            if (e[k] && idx < cap) {
-                const double d = (double)a[k] - (double)b[k];
-                acc += __builtin_fabs(d);
+        for (int k = 0; k < kPT4; ++k) {
+            if (e[k]) {
+                if (idx < cap) acc += __builtin_fabs((double)a[k] - (double)b[k]);
+                ++idx;
             }
-            row_base += (int64_t)__popcll(bal[k]);
         }
-        m = total;
-        __syncthreads();
+        m += total;
     }
     const double ws = wave_sum_f64(acc);
     if (lane == 0) wacc[wave] = ws;
