@@ -175,6 +175,17 @@ def test_edge_shapes(pace, case, mask_frac, fused):
     assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), case)
 
 
+@pytest.mark.parametrize("n", [8192, 8193])
+@FUSED
+def test_pool_at_rank_limit(pace, n, fused):
+    """8192 trajectories take the rank-and-piece kernels in the fused call,
+    8193 the separate ones."""
+    lens = np.random.default_rng(n).integers(0, 700, size=n)
+    pool = poolgen.make_custom_pool(lens, V=80, seed=n, mask_frac=0.1, W=512)
+    say("n=%d fused %s" % (n, fused))
+    assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), "n=%d" % n)
+
+
 @FUSED
 def test_pool_above_register_capacity(pace, fused):
     """20000 trajectories: the fused call falls back to the separate kernels."""
@@ -291,7 +302,7 @@ def test_select_brute_force_small(pace):
                 _select_both(pace, sc, b)
 
 
-@pytest.mark.parametrize("n", [1023, 1024, 1025, 4096, 4097, 16384, 16385, 50000])
+@pytest.mark.parametrize("n", [1023, 1024, 1025, 4096, 4097, 8192, 8193, 16384, 16385, 50000])
 def test_select_sizes_and_ties(pace, n):
     rng = np.random.default_rng(n)
     say("select n=%d" % n)
