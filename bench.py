@@ -356,6 +356,29 @@ def main():
     wall_rot = time.perf_counter() - t_rot
     rot_ms = rev[0].elapsed_time(rev[1]) / K
     assert all(int(s_.n_kept_tokens.item()) == n_keep_tok for _, _, s_ in rot)
+    # The same rotation as HIP graph replays: each copy's step captured once
+    # (the budget is fixed at capture; this pool's occupancy does not change),
+    # the K replays back to back between one event pair.
+    graphs = []
+    for t_, c_, s_ in rot:
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            s_.r_hat = 0.0
+            s_.run(t_, off, comp, pool.V, pool.occupancy, pool.capacity, c_, prefix, window, fused=True)
+        graphs.append(g)
+    for k in range(2 * R):
+        graphs[k % R].replay()
+    gv = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)
+    gv[0].record(stream)
+    for k in range(K):
+        graphs[k % R].replay()
+    gv[1].record(stream)
+    torch.cuda.synchronize()
+    graph_ms = gv[0].elapsed_time(gv[1]) / K
+    assert all(int(s_.n_kept_tokens.item()) == n_keep_tok for _, _, s_ in rot)
+    del graphs
     # the same rotation with each kernel timed by its own events: its reduce
     # time against the flushed one shows whether the steps really start cold
     rk = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in PHASES]
@@ -485,6 +508,8 @@ def main():
         "timing": "%d steps back to back between one event pair, over %d rotating pool copies "
                   "(each step's traffic exceeds the MALL, so every step starts cold); host enqueue %.2f ms "
                   "of %.2f ms wall" % (K, R, t_enq * 1e3, wall_rot * 1e3),
+        "graph_rotation_ms_per_step": graph_ms,
+        "graph_timing": "the same rotation with each copy's step captured once in a HIP graph and replayed",
         "flushed_ms_per_step": float(per_step.mean()),
         "rotation_kernel_us_mean": rot_kernel_us,
         "flushed_ms_p10_p50_p90": [float(np.percentile(per_step, q)) for q in (10, 50, 90)],
