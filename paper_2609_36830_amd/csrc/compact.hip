@@ -1,7 +1,7 @@
 // pace_compact kernels for gfx950: pack the kept trajectories' token spans
 // into the training batch (Algorithm 1), survivors in pool order.
 //
-// Copy routine (both paths): a wave copies a contiguous range of output
+// Copy routine of the scan path: a wave copies a contiguous range of output
 // elements. Output goes out as aligned 16-byte non-temporal vectors (64 lanes
 // x 16 B = 1 KiB per wave window, four windows in flight); sources are read
 // with plain loads, since the kept spans are often still in the last-level
@@ -18,12 +18,14 @@
 // written the kept count, kept tokens and the number of pieces of at most
 // kPieceLen tokens the kept spans cut into. The copy kernel then runs one
 // 256-thread workgroup per block, writing that block's packed offsets, kept
-// ids and rejected ids, and one per piece: the workgroup scans the block
-// partials (at most 512) to find its block, the 16 trajectories of the block
-// to find its span, and copies the piece with 16-byte vectors (source loads
-// dword-aligned, stores aligned and non-temporal). Pieces are short enough
-// that long trajectories spread over many workgroups, long enough that the
-// per-workgroup set-up is small next to the copy.
+// ids and rejected ids, and piece workgroups (at most one resident round;
+// each takes pieces q, q + stride, ...): the workgroup scans the block
+// partials (at most 512) to find a piece's block, the 16 trajectories of the
+// block to find its span, and copies the piece with 16-byte vectors, four
+// loads in flight per thread (source loads dword-aligned, stores aligned and
+// non-temporal). Pieces are short enough that long trajectories spread over
+// many workgroups, long enough that the per-workgroup set-up is small next to
+// the copy.
 //
 // Scan path (larger pools): one workgroup scans the flags into the packed
 // offsets, kept ids, span sources and a map from each output chunk of

@@ -36,7 +36,6 @@ constexpr int kVec = 4;                       // tags per lane per window
 constexpr int kWin = kWave * kVec;            // 256 tokens per wave window
 constexpr int kUnroll = 8;                    // windows per super-window
 constexpr int kSub = 4;                       // windows per fast-path / walk block
-constexpr bool kDoubleBuffer = false;         // two super-windows in flight
 constexpr int kWavesPerBlock = 4;
 static_assert(kScoreChunkAlign % (kWin * kUnroll) == 0, "chunk must be a multiple of the super-window");
 
@@ -106,7 +105,7 @@ __device__ __forceinline__ void load_super(const int32_t *__restrict__ tags, int
 
 // kNarrow: every tag + 1 < 2^24, so a lane's 32 tags of one super-window sum
 // below 2^29 in 32 bits before widening.
-template <bool kNarrow, bool kVecLoad, int U = kUnroll, bool kDouble = kDoubleBuffer>
+template <bool kNarrow, bool kVecLoad, int U = kUnroll>
 __global__ __launch_bounds__(256) void score_reduce_kernel(
     const int32_t *__restrict__ tags, const int64_t *__restrict__ off, int64_t n, int64_t NT,
     int64_t chunk_len, int64_t n_chunks, uint64_t *__restrict__ part_sum,
@@ -118,14 +117,11 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
     const int64_t cs = chunk * chunk_len;
     const int64_t ce = (cs + chunk_len < NT) ? cs + chunk_len : NT;
 
-    // The first super-window's loads (the first two, double-buffered) do not
-    // depend on the trajectory search: issue them first so the search latency
-    // hides under them. Double-buffered, the next super-window is in flight
-    // while one is summed.
+    // The first super-window's loads do not depend on the trajectory search:
+    // issue them first so the search latency hides under them.
     constexpr int64_t kSuper = (int64_t)kWin * U;
-    int4 va[U], vb[kDouble ? U : 1];
+    int4 va[U];
     load_super<kVecLoad>(tags, cs, ce, lane, va);
-    if (kDouble && cs + kSuper < ce) load_super<kVecLoad>(tags, cs + kSuper, ce, lane, vb);
 
     // Trajectory that contains the chunk's first token. First guess: the
     // 64 offsets around the position the token would have if all
@@ -277,19 +273,9 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
         }
     };
 
-    if constexpr (kDouble) {
-        for (int64_t pos = cs; pos < ce; pos += 2 * kSuper) {
-            process(va, pos);
-            if (pos + 2 * kSuper < ce) load_super<kVecLoad>(tags, pos + 2 * kSuper, ce, lane, va);
-            if (pos + kSuper >= ce) break;
-            process(vb, pos + kSuper);
-            if (pos + 3 * kSuper < ce) load_super<kVecLoad>(tags, pos + 3 * kSuper, ce, lane, vb);
-        }
-    } else {
-        for (int64_t pos = cs; pos < ce; pos += kSuper) {
-            if (pos != cs) load_super<kVecLoad>(tags, pos, ce, lane, va);
-            process(va, pos);
-        }
+    for (int64_t pos = cs; pos < ce; pos += kSuper) {
+        if (pos != cs) load_super<kVecLoad>(tags, pos, ce, lane, va);
+        process(va, pos);
     }
     if (pending) flush();
     if (lane < n_held) store_piece(held_at, held_s, held_c);
