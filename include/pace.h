@@ -351,7 +351,8 @@ int pace_stale_k(const int64_t *gen_sum, const int64_t *gen_count, const int32_t
  * hist_out: int64 [3][2][nbins + 2]: [metric][0 rejected, 1 retained][bin],
  *   bin 0 below the first edge, nbins + 1 at or above the last.
  * totals_out: int64 [2][4]: per class, count, sum of (j - c), sum S, sum T.
- * One workgroup; outputs are overwritten, not accumulated. */
+ * Four workgroups (one per metric, one for the totals); outputs are
+ * overwritten, not accumulated. */
 int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t *gen_count,
                      const int32_t *completion, int32_t current_version, const uint8_t *keep, int64_t n_traj,
                      const double *edges, int nbins, int64_t *hist_out, int64_t *totals_out, void *stream);

@@ -84,3 +84,44 @@ def test_diagnostics_pools(pace, name):
         h, t = pace.pace_diagnostics(sc, S, T, comp, pool.V, keep, D(edges))
         oh, ot = oracle.diagnostics(pool.tags, pool.offsets, pool.completion, pool.V, osc, okeep, edges)
         assert np.array_equal(H(h), oh) and np.array_equal(H(t), ot)
+
+
+def _direct_pool(rng, n, V=40):
+    """Short trajectories (0..6 tokens) with tags in [c - 9, c] or -1."""
+    lens = rng.integers(0, 7, n).astype(np.int64)
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    comp = rng.integers(0, V + 1, n).astype(np.int32)
+    owner = np.repeat(np.arange(n), lens)
+    c_tok = comp[owner].astype(np.int64)
+    tags = np.maximum(c_tok - rng.integers(0, 10, owner.size), 0).astype(np.int32)
+    tags[rng.random(owner.size) < 0.2] = -1
+    return tags, off, comp
+
+
+@pytest.mark.parametrize("n", [0, 1, 5, 1023, 1025, 4097, 10001])
+def test_diagnostics_shapes(pace, n):
+    """Empty, sub-round and several-round pools; NaN and infinite scores,
+    scores and metrics exactly on edges, repeated edges, keep bytes above 1
+    (retained), and bin counts from 1 to the maximum."""
+    rng = np.random.default_rng(1000 + n)
+    V = 40
+    tags, off, comp = _direct_pool(rng, n, V)
+    sc, S, T = pace.pace_score(D(tags), D(off), D(comp), V)
+    osc, _, _ = oracle.score(tags, off, comp, V)
+    assert np.array_equal(H(sc).view(np.uint64), osc.view(np.uint64))
+    score = osc.copy()
+    if n:
+        pick = rng.integers(0, n, max(1, n // 7))
+        score[pick] = rng.choice([np.nan, np.inf, -np.inf, 0.0, 3.0, 12.0], pick.size)
+    keep = rng.choice(np.array([0, 1, 2, 255], np.uint8), n)
+    for nb in (1, 2, 63, 64, 1023, 1024):
+        if nb in (2, 63):
+            # repeated edges, integer-valued so that K_wait lands on them
+            base = np.sort(rng.integers(0, 13, nb + 1)).astype(np.float64)
+            edges = np.array([base] * 3)
+        else:
+            edges = np.sort(rng.uniform(-1, 30, (3, nb + 1)), axis=1)
+        say("diagnostics direct n=%d nbins=%d" % (n, nb))
+        h, t = pace.pace_diagnostics(D(score), S, T, D(comp), V, D(keep), D(edges))
+        oh, ot = oracle.diagnostics(tags, off, comp, V, score, keep, edges)
+        assert np.array_equal(H(h), oh) and np.array_equal(H(t), ot)
