@@ -555,6 +555,8 @@ def main():
         t_cpu = time.perf_counter() - ts
         out["cpu_baseline"] = {
             "value": reps * pool.n_tokens / t_cpu, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "trajectories_per_s": reps * pool.n / t_cpu, "GBps": reps * B / t_cpu / 1e9,
+            "ms_per_step": t_cpu / reps * 1e3,
             "sample": "%d full oracle filter steps (score, budget, select, compact) on the same "
                       "%s pool, single-threaded C, %.1f s, on %s (%d host threads visible)"
                       % (reps, args.config, t_cpu, cpu_model(), os.cpu_count() or 0),
