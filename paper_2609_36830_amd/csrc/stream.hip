@@ -40,6 +40,13 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
     __shared__ double s_kappa;
     __shared__ int64_t s_state[2];
     const int t = threadIdx.x;
+    // The first tile's scores do not depend on the cutoff: their loads go
+    // out first (a slot past the end reads the last score and is dropped).
+    double sc[kSItems];
+    if (n > 0) {
+#pragma unroll
+        for (int q = 0; q < kSItems; ++q) sc[q] = score[min((int64_t)t * kSItems + q, n - 1)];
+    }
     if (t == 0) {
         s_state[0] = state[0];
         s_state[1] = state[1];
@@ -51,20 +58,34 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
 
     // 1. The cutoff, from the window as it stands before this draw (the cnt
     //    most recent entries end just before head).
-    for (int64_t u = t; u < cnt; u += kST) win[u] = ring[(head - cnt + u + cap) % cap];
+    for (int64_t u = t; u < cnt; u += kST) {
+        const int64_t at = head - cnt + u;        // in [-cap, cap): head < cap, u < cnt <= cap
+        win[u] = ring[at < 0 ? at + cap : at];
+    }
     __syncthreads();
     if (cnt >= window_min && cnt > 0 && rate > 0.0) {
         const double p = 1.0 - rate;
         int64_t k = (int64_t)ceil(p * (double)cnt);
         if (k < 1) k = 1;
-        for (int64_t u = t; u < cnt; u += kST) {
-            const double x = win[u];
-            int64_t r = 0;
-            for (int64_t v = 0; v < cnt; ++v) {
-                const double y = win[v];
-                r += (y < x || (y == x && v < u)) ? 1 : 0;
-            }
-            if (r == k - 1) s_kappa = x;
+        // P adjacent lanes share an entry, each counting over a 1/P slice of
+        // the window (P = 8, 4, 2 or 1, as many as the threads allow); the
+        // lanes' counts are added by shuffles.
+        const int P = (8 * cnt <= kST) ? 8 : (4 * cnt <= kST) ? 4 : (2 * cnt <= kST) ? 2 : 1;
+        const int sub = t & (P - 1);
+        const int64_t slice = (cnt + P - 1) / P;
+        const int64_t v0 = sub * slice, v1 = (v0 + slice < cnt) ? v0 + slice : cnt;
+        for (int64_t u0 = 0; u0 < cnt; u0 += kST / P) {
+            const int64_t u = u0 + t / P;
+            const bool has = u < cnt;
+            const double x = has ? win[u] : 0.0;
+            uint32_t r = 0;
+            if (has)
+                for (int64_t v = v0; v < v1; ++v) {
+                    const double y = win[v];
+                    r += (y < x || (y == x && v < u)) ? 1u : 0u;
+                }
+            for (int o = 1; o < P; o <<= 1) r += (uint32_t)__shfl_xor((int)r, o, kWave);
+            if (has && sub == 0 && (int64_t)r == k - 1) s_kappa = x;
         }
         __syncthreads();
     }
@@ -76,10 +97,14 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
         const int64_t i0 = base + (int64_t)t * kSItems;
         bool in[kSItems], ret[kSItems];
         uint32_t c = 0;
+        if (base > 0) {
+#pragma unroll
+            for (int q = 0; q < kSItems; ++q) sc[q] = score[min(i0 + q, n - 1)];
+        }
 #pragma unroll
         for (int q = 0; q < kSItems; ++q) {
             in[q] = i0 + q < n;
-            ret[q] = in[q] && !(score[i0 + q] > kappa);
+            ret[q] = in[q] && !(sc[q] > kappa);
             c += ret[q] ? 1u : 0u;
         }
         uint32_t tot;
