@@ -286,7 +286,8 @@ int pace_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t 
  * reject_ids_out: int32, the rejected ids ascending (n_traj entries suffice).
  * kappa_out: f64 device scalar. counts_out: int64 [3] device: drawn,
  *   retained, rejected.
- * One workgroup; no workspace. */
+ * Two kernels: the cutoff, over ceil(window_cap / 16) workgroups, writes
+ * kappa_out, which the draw (one workgroup) then reads; no workspace. */
 int pace_stream_admit(const double *score, int64_t n_traj, double r_hat, const pace_params *params,
                       int64_t batch_size, double *window_ring, int64_t window_cap, int64_t *window_state,
                       uint8_t *status_out, uint8_t *keep_out, int32_t *reject_ids_out, double *kappa_out,
@@ -368,7 +369,8 @@ int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t 
  *   single-workgroup select of large pools, or the streaming draw),
  *   PACE_PHASE_COMPACT (the compaction copy kernel), PACE_PHASE_PREFIX (the
  *   Prefix Forgetting Score kernel), PACE_PHASE_AUX (the single kernel of
- *   pace_group_score, pace_group_expand, pace_stale_k or pace_diagnostics).
+ *   pace_group_score, pace_group_expand, pace_stale_k or pace_diagnostics,
+ *   or the window-cutoff kernel of the streaming rule).
  * start_event, stop_event: hipEvent_t handles created by the caller with
  *   timing enabled; both NULL disarms the phase. The caller keeps ownership.
  * Returns PACE_ERR_INVALID_ARG for an unknown phase or one NULL event. */

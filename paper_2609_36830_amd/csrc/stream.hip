@@ -3,21 +3,26 @@
 // observed scores; the trainer draws candidates in pool order, rejects those
 // scoring above kappa and retains the rest until the batch is full.
 //
-// One workgroup of 1024 threads:
-//   1. the window (at most kStreamWindowMax entries) goes to LDS; kappa is
-//      its ceil(p * cnt)-th smallest entry, p = 1 - rate (the lower empirical
-//      quantile), found by ranking every entry against all others (ties by
-//      position); with fewer than window_min entries or a rate of 0 it is
-//      +inf;
-//   2. the draw needs no sequential walk: candidate i is drawn iff fewer
-//      than batch_size candidates before it are retained, so one ordered
-//      count of the retained flags (block scans over tiles of the pool)
-//      gives every candidate's status, the rejected ids in order
-//      (i minus the retained before i) and the draw length;
-//   3. the drawn scores enter the ring in draw order (only the last `cap`
-//      of them can survive), and the ring state is advanced.
+// Two kernels:
+//   1. stream_kappa: kappa is the ceil(p * cnt)-th smallest of the cnt window
+//      entries, p = 1 - rate (the lower empirical quantile), or +inf with
+//      fewer than window_min entries or a rate of 0. Each workgroup ranks
+//      kKQ entries against the whole window (one entry per thread) in the
+//      total order (score key, position), so exactly one entry has rank
+//      k - 1 and exactly one thread writes kappa; spread over the chip, the
+//      cnt^2 comparisons cost a few microseconds instead of the twenty one
+//      workgroup needs for them;
+//   2. stream_admit, one workgroup of 1024 threads:
+//      a. the draw needs no sequential walk: candidate i is drawn iff fewer
+//         than batch_size candidates before it are retained, so one ordered
+//         count of the retained flags (block scans over tiles of the pool)
+//         gives every candidate's status, the rejected ids in order (i minus
+//         the retained before i) and the draw length;
+//      b. the drawn scores enter the ring in draw order (only the last `cap`
+//         of them can survive), and the ring state is advanced.
 #include "device_util.hpp"
 #include "kernels.hpp"
+#include "select_block.hpp"
 
 #pragma clang fp contract(off)
 
@@ -30,18 +35,68 @@ constexpr int kSNW = kST / kWave;
 constexpr int kSItems = 8;
 constexpr int64_t kSTile = (int64_t)kST * kSItems;
 
+constexpr int kKQ = 16;    // window entries ranked per workgroup
+
+__global__ __launch_bounds__(kST) void stream_kappa_kernel(const double *__restrict__ ring, int64_t cap,
+                                                           const int64_t *__restrict__ state, double rate,
+                                                           int64_t window_min, double *__restrict__ kappa_out) {
+    static_assert(kStreamWindowMax <= kST, "one window entry per thread");
+    __shared__ uint32_t part[kSNW][kKQ / 4];
+    const int t = threadIdx.x, lane = lane_id(), wave = t / kWave;
+    const int64_t head = clamp64(state[0], 0, cap - 1);
+    const int64_t cnt = clamp64(state[1], 0, cap);
+    if (!(cnt >= window_min && cnt > 0 && rate > 0.0)) {
+        if (blockIdx.x == 0 && t == 0) *kappa_out = __builtin_inf();
+        return;
+    }
+    const int64_t u0 = (int64_t)blockIdx.x * kKQ;
+    if (u0 >= cnt) return;                          // the whole workgroup
+    // Window entry u (0 = oldest): the cnt most recent entries end just
+    // before head.
+    auto at = [&](int64_t u) {
+        const int64_t x = head - cnt + u;           // in [-cap, cap)
+        return x < 0 ? x + cap : x;
+    };
+    const bool mine = t < cnt;
+    const uint64_t ky = score_key(ring[at(mine ? t : cnt - 1)]);
+    const uint64_t kq_lane = score_key(ring[at(min(u0 + (lane < kKQ ? lane : 0), cnt - 1))]);
+    // Entries before query q in (key, position) order, one bit per thread,
+    // packed four queries per word (a wave's count fits 8 bits).
+    uint32_t packed[kKQ / 4] = {};
+#pragma unroll
+    for (int q = 0; q < kKQ; ++q) {
+        const uint64_t kq = (uint64_t)readlane_i64((int64_t)kq_lane, q);
+        const uint32_t before = (uint32_t)(mine & ((ky < kq) | ((ky == kq) & ((int64_t)t < u0 + q))));
+        packed[q / 4] += before << (8 * (q % 4));
+    }
+#pragma unroll
+    for (int w = 0; w < kKQ / 4; ++w) {
+        const uint32_t sum = (uint32_t)readlane_i32((int32_t)wave_incl_scan_u32(packed[w]), kWave - 1);
+        if (lane == 0) part[wave][w] = sum;
+    }
+    __syncthreads();
+    if (t < kKQ) {
+        uint32_t r = 0;
+#pragma unroll
+        for (int v = 0; v < kSNW; ++v) r += (part[v][t / 4] >> (8 * (t % 4))) & 0xffu;
+        const double p = 1.0 - rate;
+        int64_t k = (int64_t)ceil(p * (double)cnt);
+        if (k < 1) k = 1;
+        const int64_t u = u0 + t;
+        if (u < cnt && (int64_t)r == k - 1) *kappa_out = ring[at(u)];
+    }
+}
+
 __global__ __launch_bounds__(kST) void stream_admit_kernel(
-    const double *__restrict__ score, int64_t n, double rate, int64_t window_min, int64_t B,
+    const double *__restrict__ score, int64_t n, int64_t B,
     double *__restrict__ ring, int64_t cap, int64_t *__restrict__ state, uint8_t *__restrict__ status,
-    uint8_t *__restrict__ keep, int32_t *__restrict__ reject_ids, double *__restrict__ kappa_out,
+    uint8_t *__restrict__ keep, int32_t *__restrict__ reject_ids, const double *__restrict__ kappa_in,
     int64_t *__restrict__ counts) {
-    __shared__ double win[kStreamWindowMax];
     __shared__ uint32_t wsum[kSNW];
-    __shared__ double s_kappa;
     __shared__ int64_t s_state[2];
     const int t = threadIdx.x;
-    // The first tile's scores do not depend on the cutoff: their loads go
-    // out first (a slot past the end reads the last score and is dropped).
+    // The first tile's scores, the cutoff and the ring state are loaded
+    // together (a slot past the end reads the last score and is dropped).
     double sc[kSItems];
     if (n > 0) {
 #pragma unroll
@@ -50,48 +105,13 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
     if (t == 0) {
         s_state[0] = state[0];
         s_state[1] = state[1];
-        s_kappa = __builtin_inf();
     }
+    const double kappa = *kappa_in;            // written by stream_kappa
     __syncthreads();
     const int64_t head = clamp64(s_state[0], 0, cap - 1);
     const int64_t cnt = clamp64(s_state[1], 0, cap);
 
-    // 1. The cutoff, from the window as it stands before this draw (the cnt
-    //    most recent entries end just before head).
-    for (int64_t u = t; u < cnt; u += kST) {
-        const int64_t at = head - cnt + u;        // in [-cap, cap): head < cap, u < cnt <= cap
-        win[u] = ring[at < 0 ? at + cap : at];
-    }
-    __syncthreads();
-    if (cnt >= window_min && cnt > 0 && rate > 0.0) {
-        const double p = 1.0 - rate;
-        int64_t k = (int64_t)ceil(p * (double)cnt);
-        if (k < 1) k = 1;
-        // P adjacent lanes share an entry, each counting over a 1/P slice of
-        // the window (P = 8, 4, 2 or 1, as many as the threads allow); the
-        // lanes' counts are added by shuffles.
-        const int P = (8 * cnt <= kST) ? 8 : (4 * cnt <= kST) ? 4 : (2 * cnt <= kST) ? 2 : 1;
-        const int sub = t & (P - 1);
-        const int64_t slice = (cnt + P - 1) / P;
-        const int64_t v0 = sub * slice, v1 = (v0 + slice < cnt) ? v0 + slice : cnt;
-        for (int64_t u0 = 0; u0 < cnt; u0 += kST / P) {
-            const int64_t u = u0 + t / P;
-            const bool has = u < cnt;
-            const double x = has ? win[u] : 0.0;
-            uint32_t r = 0;
-            if (has)
-                for (int64_t v = v0; v < v1; ++v) {
-                    const double y = win[v];
-                    r += (y < x || (y == x && v < u)) ? 1u : 0u;
-                }
-            for (int o = 1; o < P; o <<= 1) r += (uint32_t)__shfl_xor((int)r, o, kWave);
-            if (has && sub == 0 && (int64_t)r == k - 1) s_kappa = x;
-        }
-        __syncthreads();
-    }
-    const double kappa = s_kappa;
-
-    // 2. The draw.
+    // a. The draw.
     int64_t run_ret = 0, drawn = 0;
     for (int64_t base = 0; base < n; base += kSTile) {
         const int64_t i0 = base + (int64_t)t * kSItems;
@@ -133,13 +153,12 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
     }
     const int64_t retained = run_ret < B ? run_ret : B;
 
-    // 3. The window takes the drawn scores, oldest first.
+    // b. The window takes the drawn scores, oldest first.
     const int64_t first = drawn > cap ? drawn - cap : 0;
     for (int64_t u = first + t; u < drawn; u += kST) ring[(head + u) % cap] = score[u];
     if (t == 0) {
         state[0] = (head + drawn) % cap;
         state[1] = (cnt + drawn < cap) ? cnt + drawn : cap;
-        *kappa_out = kappa;
         counts[0] = drawn;
         counts[1] = retained;
         counts[2] = drawn - retained;
@@ -151,8 +170,11 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
 hipError_t launch_stream_admit(const double *score, int64_t n, double rate, int64_t window_min, int64_t B,
                                double *ring, int64_t cap, int64_t *state, uint8_t *status, uint8_t *keep,
                                int32_t *reject_ids, double *kappa, int64_t *counts, hipStream_t stream) {
-    return launch(kPhaseSelect, stream_admit_kernel, dim3(1), dim3(kST), stream, score, n, rate, window_min, B,
-                  ring, cap, state, status, keep, reject_ids, kappa, counts);
+    hipError_t e = launch(kPhaseAux, stream_kappa_kernel, dim3((unsigned)((cap + kKQ - 1) / kKQ)), dim3(kST), stream,
+                          ring, cap, state, rate, window_min, kappa);
+    if (e != hipSuccess) return e;
+    return launch(kPhaseSelect, stream_admit_kernel, dim3(1), dim3(kST), stream, score, n, B, ring, cap, state,
+                  status, keep, reject_ids, (const double *)kappa, counts);
 }
 
 }  // namespace pace
