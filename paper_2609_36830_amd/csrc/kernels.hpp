@@ -188,9 +188,12 @@ hipError_t launch_group_filter_step(const int32_t *tags, const int64_t *offsets,
 
 // ---- streaming admission rule ------------------------------------------------
 constexpr int64_t kStreamWindowMax = 1024;   // largest score window (ring entries)
+// With offsets and parts.cnt non-null, the draw also writes the compaction's
+// block partials of its keep flags (offsets clamped to [0, n_tokens]).
 hipError_t launch_stream_admit(const double *score, int64_t n, double rate, int64_t window_min, int64_t B,
                                double *ring, int64_t cap, int64_t *state, uint8_t *status, uint8_t *keep,
-                               int32_t *reject_ids, double *kappa, int64_t *counts, hipStream_t stream);
+                               int32_t *reject_ids, double *kappa, int64_t *counts, const int64_t *offsets,
+                               int64_t n_tokens, const PieceParts &parts, hipStream_t stream);
 
 // ---- Prefix Forgetting Score --------------------------------------------------
 hipError_t launch_prefix_score(const float *lp_new, const float *lp_beh, const int32_t *tags,

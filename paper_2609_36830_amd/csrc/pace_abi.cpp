@@ -373,7 +373,7 @@ int pace_stream_admit(const double *score, int64_t n_traj, double r_hat, const p
     const double rate = r_hat < p.r_max ? r_hat : p.r_max;
     return hip_status(launch_stream_admit(score, n_traj, rate, p.window_min, batch_size, window_ring,
                                           window_cap, window_state, status_out, keep_out, reject_ids_out,
-                                          kappa_out, counts_out, (hipStream_t)stream));
+                                          kappa_out, counts_out, nullptr, 0, PieceParts{}, (hipStream_t)stream));
 }
 
 int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
@@ -417,14 +417,25 @@ int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
     hipError_t e = launch_score(tags, offsets, n_traj, n_tokens, completion, current_version, prefix_score,
                                 window_sorted, window_n, use_prefix, p.w_wait, p.gamma, score_out, gen_sum_out,
                                 gen_count_out, sws, aligned(tags, 16), st);
+    // Pools the piece compaction takes get their block partials from the
+    // draw itself; the kept trajectories are at most min(batch_size, n).
+    const bool pieces = compact_piece_ok(n_traj, n_tokens);
+    const CompactWs cw = compact_ws_carve(cws, n_traj, n_tokens);
     if (e == hipSuccess) {
         const double rate = r_hat < p.r_max ? r_hat : p.r_max;
         e = launch_stream_admit(score_out, n_traj, rate, p.window_min, batch_size, window_ring, window_cap,
-                                window_state, status_out, keep_out, reject_ids_out, kappa_out, counts_out, st);
+                                window_state, status_out, keep_out, reject_ids_out, kappa_out, counts_out,
+                                pieces ? offsets : nullptr, n_tokens, pieces ? cw.parts : PieceParts{}, st);
     }
-    if (e == hipSuccess)
-        e = launch_compact(offsets, n_traj, n_tokens, keep_out, cols, n_cols, offsets_out, kept_ids_out,
-                           n_kept_tokens_out, cws, st);
+    if (e == hipSuccess) {
+        if (pieces)
+            e = launch_compact_pieces(offsets, n_traj, n_tokens, keep_out, cw.parts, cols, n_cols, offsets_out,
+                                      kept_ids_out, n_kept_tokens_out, nullptr, 0,
+                                      batch_size < n_traj ? batch_size : n_traj, st);
+        else
+            e = launch_compact(offsets, n_traj, n_tokens, keep_out, cols, n_cols, offsets_out, kept_ids_out,
+                               n_kept_tokens_out, cws, st);
+    }
     rc = hip_status(e);
     if (rc != PACE_OK) return rc;
     *r_hat_inout = r_hat;

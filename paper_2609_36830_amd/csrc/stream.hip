@@ -87,21 +87,63 @@ __global__ __launch_bounds__(kST) void stream_kappa_kernel(const double *__restr
     }
 }
 
+__device__ __forceinline__ int64_t shfl_xor_i64(int64_t v, int m) {
+    const int lo = __shfl_xor((int)(uint32_t)v, m, kWave);
+    const int hi = __shfl_xor((int)(uint32_t)((uint64_t)v >> 32), m, kWave);
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// kParts: also writes the compaction's block partials of the keep flags
+// (kept count, kept tokens, pieces per block of kPieceBlock trajectories,
+// lengths from offsets clamped to [0, NT]); a block is two adjacent threads.
+template <bool kParts>
 __global__ __launch_bounds__(kST) void stream_admit_kernel(
     const double *__restrict__ score, int64_t n, int64_t B,
     double *__restrict__ ring, int64_t cap, int64_t *__restrict__ state, uint8_t *__restrict__ status,
     uint8_t *__restrict__ keep, int32_t *__restrict__ reject_ids, const double *__restrict__ kappa_in,
-    int64_t *__restrict__ counts) {
+    int64_t *__restrict__ counts, const int64_t *__restrict__ off, int64_t NT, PieceParts parts, bool vec) {
+    static_assert(2 * kSItems == kPieceBlock && kSTile % kPieceBlock == 0, "a block is two threads' items");
     __shared__ uint32_t wsum[kSNW];
     __shared__ int64_t s_state[2];
     const int t = threadIdx.x;
     // The first tile's scores, the cutoff and the ring state are loaded
     // together (a slot past the end reads the last score and is dropped).
     double sc[kSItems];
-    if (n > 0) {
+    int64_t ob[kSItems + 1];                   // clamped offsets of this thread's items (kParts)
+    // A wave whose items all lie in the pool reads each thread's run as
+    // 16-byte vectors (vec: both arrays 16-byte aligned); element loads,
+    // clamped to the pool, otherwise. (One element per load, the lanes 64
+    // bytes apart, would leave the single CU bound on address processing.)
+    const int wave = __builtin_amdgcn_readfirstlane(t / kWave);
+    auto load_tile = [&](int64_t base) {
+        const int64_t i0 = base + (int64_t)t * kSItems;
+        const bool full = vec && base + (int64_t)(wave + 1) * kWave * kSItems <= n;
+        if (full) {
 #pragma unroll
-        for (int q = 0; q < kSItems; ++q) sc[q] = score[min((int64_t)t * kSItems + q, n - 1)];
-    }
+            for (int j = 0; j < kSItems / 2; ++j) {
+                const double2 v = *reinterpret_cast<const double2 *>(score + i0 + 2 * j);
+                sc[2 * j] = v.x;
+                sc[2 * j + 1] = v.y;
+            }
+            if constexpr (kParts) {
+#pragma unroll
+                for (int j = 0; j < kSItems / 2; ++j) {
+                    const longlong2 v = *reinterpret_cast<const longlong2 *>(off + i0 + 2 * j);
+                    ob[2 * j] = clamp64(v.x, 0, NT);
+                    ob[2 * j + 1] = clamp64(v.y, 0, NT);
+                }
+                ob[kSItems] = clamp64(off[i0 + kSItems], 0, NT);     // i0 + kSItems <= n
+            }
+        } else {
+#pragma unroll
+            for (int q = 0; q < kSItems; ++q) sc[q] = score[min(i0 + q, n - 1)];
+            if constexpr (kParts) {
+#pragma unroll
+                for (int q = 0; q <= kSItems; ++q) ob[q] = clamp64(off[min(i0 + q, n)], 0, NT);
+            }
+        }
+    };
+    if (n > 0) load_tile(0);
     if (t == 0) {
         s_state[0] = state[0];
         s_state[1] = state[1];
@@ -117,10 +159,7 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
         const int64_t i0 = base + (int64_t)t * kSItems;
         bool in[kSItems], ret[kSItems];
         uint32_t c = 0;
-        if (base > 0) {
-#pragma unroll
-            for (int q = 0; q < kSItems; ++q) sc[q] = score[min(i0 + q, n - 1)];
-        }
+        if (base > 0) load_tile(base);
 #pragma unroll
         for (int q = 0; q < kSItems; ++q) {
             in[q] = i0 + q < n;
@@ -131,6 +170,8 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
         const uint32_t before = block_excl_sum_u32<kSNW>(c, tot, wsum);
         int64_t rb = run_ret + before;          // retained before item i0 + q
         uint32_t d = 0;
+        uint32_t k_cnt = 0, k_pcs = 0;
+        int64_t k_len = 0;
 #pragma unroll
         for (int q = 0; q < kSItems; ++q) {
             if (!in[q]) continue;
@@ -145,6 +186,26 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
             status[i] = st;
             keep[i] = st == 1 ? 1 : 0;
             rb += ret[q] ? 1 : 0;
+            if constexpr (kParts) {
+                if (st == 1) {
+                    const int64_t len = ob[q + 1] > ob[q] ? ob[q + 1] - ob[q] : 0;
+                    k_cnt += 1;
+                    k_len += len;
+                    k_pcs += (uint32_t)((len + kPieceLen - 1) / kPieceLen);
+                }
+            }
+        }
+        if constexpr (kParts) {
+            const uint32_t c2 = k_cnt + (uint32_t)__shfl_xor((int)k_cnt, 1, kWave);
+            const uint32_t p2 = k_pcs + (uint32_t)__shfl_xor((int)k_pcs, 1, kWave);
+            const int64_t l2 = k_len + shfl_xor_i64(k_len, 1);
+            const int64_t b0 = base + (int64_t)(t & ~1) * kSItems;     // the block's first trajectory
+            if ((t & 1) == 0 && b0 < n) {
+                const int64_t blk = b0 / kPieceBlock;
+                parts.cnt[blk] = (int32_t)c2;
+                parts.len[blk] = l2;
+                parts.pcs[blk] = (int32_t)p2;
+            }
         }
         uint32_t dtot;
         (void)block_excl_sum_u32<kSNW>(d, dtot, wsum);
@@ -169,12 +230,18 @@ __global__ __launch_bounds__(kST) void stream_admit_kernel(
 
 hipError_t launch_stream_admit(const double *score, int64_t n, double rate, int64_t window_min, int64_t B,
                                double *ring, int64_t cap, int64_t *state, uint8_t *status, uint8_t *keep,
-                               int32_t *reject_ids, double *kappa, int64_t *counts, hipStream_t stream) {
+                               int32_t *reject_ids, double *kappa, int64_t *counts, const int64_t *offsets,
+                               int64_t n_tokens, const PieceParts &parts, hipStream_t stream) {
     hipError_t e = launch(kPhaseAux, stream_kappa_kernel, dim3((unsigned)((cap + kKQ - 1) / kKQ)), dim3(kST), stream,
                           ring, cap, state, rate, window_min, kappa);
     if (e != hipSuccess) return e;
-    return launch(kPhaseSelect, stream_admit_kernel, dim3(1), dim3(kST), stream, score, n, B, ring, cap, state,
-                  status, keep, reject_ids, (const double *)kappa, counts);
+    const bool with_parts = offsets && parts.cnt;
+    const bool vec = ((uintptr_t)score & 15) == 0 && (!with_parts || ((uintptr_t)offsets & 15) == 0);
+    if (with_parts)
+        return launch(kPhaseSelect, stream_admit_kernel<true>, dim3(1), dim3(kST), stream, score, n, B, ring, cap,
+                      state, status, keep, reject_ids, (const double *)kappa, counts, offsets, n_tokens, parts, vec);
+    return launch(kPhaseSelect, stream_admit_kernel<false>, dim3(1), dim3(kST), stream, score, n, B, ring, cap,
+                  state, status, keep, reject_ids, (const double *)kappa, counts, offsets, n_tokens, parts, vec);
 }
 
 }  // namespace pace
