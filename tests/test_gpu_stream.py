@@ -154,3 +154,50 @@ def test_stream_step_fused_matches_oracle(pace):
         assert np.array_equal(H(bufs["offsets_out"])[: okept + 1], ooff)
         assert np.array_equal(H(bufs["kept_ids"])[:okept], oids)
         assert np.array_equal(H(bufs["cols_out"][0])[:nk], opacked[0])
+
+
+@pytest.mark.parametrize("n", [1, 17, 1000, 8192, 8193, 9000])
+def test_stream_step_fused_shapes(pace, n):
+    """pace_stream_step on ragged pools: partial 16-trajectory blocks and
+    partial waves of the draw, empty and multi-piece (> 16384-token)
+    trajectories, both sides of the piece-compaction limit (8192
+    trajectories), two steps so that the second draws against a filled
+    window; every output against the oracle's chain."""
+    rng = np.random.default_rng(700 + n)
+    V = 50
+    lens = rng.integers(0, 40, n).astype(np.int64)
+    lens[rng.random(n) < 0.1] = 0
+    if n >= 17:
+        lens[rng.integers(0, n, 2)] = [20000, 40000]
+    off = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    comp = rng.integers(V - 8, V + 1, n).astype(np.int32)
+    owner = np.repeat(np.arange(n), lens)
+    tags = np.maximum(comp[owner].astype(np.int64) - rng.integers(0, 12, owner.size), 0).astype(np.int32)
+    tags[rng.random(owner.size) < 0.1] = -1
+    occupancy, capacity = n, max(1, n // 3)
+    B = int(rng.integers(1, n + 2))
+    ow = oracle.StreamWindow(256)
+    gw = pace.StreamWindow(256, DEV)
+    params = pace.default_params(window_min=4)
+    rh_o = rh_g = 0.0
+    bufs = None
+    for step in range(2):
+        say("stream step fused shapes n=%d step=%d B=%d tokens=%d" % (n, step, B, int(off[-1])))
+        bufs, rh_g = pace.pace_stream_step(D(tags), D(off), D(comp), V, occupancy, capacity, [D(tags)], gw, B,
+                                           params=params, r_hat_prev=rh_g, buffers=bufs)
+        torch.cuda.synchronize()
+        osc, _, _ = oracle.score(tags, off, comp, V)
+        _, rh_o = oracle.budget(occupancy, capacity, rh_o, 0.0, 0.9)
+        ost, okappa, odrawn, okept = oracle.stream_admit(osc, rh_o, ow, B, window_min=4)
+        ooff, oids, opacked = oracle.compact(off, (ost == 1).astype(np.uint8), [tags])
+        assert rh_g == rh_o
+        assert np.array_equal(H(bufs["score"])[:n].view(np.uint64), osc.view(np.uint64))
+        assert np.array_equal(H(bufs["status"])[:n], ost)
+        assert float(H(bufs["kappa"])[0]) == okappa
+        assert list(H(bufs["counts"])) == [odrawn, okept, odrawn - okept]
+        assert np.array_equal(H(gw.ring).view(np.uint64), ow.ring.view(np.uint64))
+        nk = int(H(bufs["n_kept_tokens"])[0])
+        assert nk == int(ooff[-1])
+        assert np.array_equal(H(bufs["offsets_out"])[: okept + 1], ooff)
+        assert np.array_equal(H(bufs["kept_ids"])[:okept], oids)
+        assert np.array_equal(H(bufs["cols_out"][0])[:nk], opacked[0])
