@@ -94,8 +94,8 @@ def reduce_traffic(config):
 
 # config -> {"sha256": digest of the score_reduce sources, "bytes": HBM bytes per launch}
 REDUCE_COUNTERS = {
-    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98153.9 KiB, WRITE_SIZE 175.8 KiB
-    "stress": {"sha256": "f08e39fb9827a71d47a05d77e52064ab4794caa43ed46ea0bc13f540b3d8af53", "bytes": 201199102},
+    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98152.6 KiB, WRITE_SIZE 175.7 KiB
+    "stress": {"sha256": "f08e39fb9827a71d47a05d77e52064ab4794caa43ed46ea0bc13f540b3d8af53", "bytes": 201196442},
 }
 
 
