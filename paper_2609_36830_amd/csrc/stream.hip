@@ -10,8 +10,8 @@
 //      kKQ entries against the whole window (one entry per thread) in the
 //      total order (score key, position), so exactly one entry has rank
 //      k - 1 and exactly one thread writes kappa; spread over the chip, the
-//      cnt^2 comparisons cost a few microseconds instead of the twenty one
-//      workgroup needs for them;
+//      cnt^2 comparisons cost a few microseconds (about twenty on a single
+//      workgroup);
 //   2. stream_admit, one workgroup of 1024 threads:
 //      a. the draw needs no sequential walk: candidate i is drawn iff fewer
 //         than batch_size candidates before it are retained, so one ordered
@@ -19,7 +19,9 @@
 //         gives every candidate's status, the rejected ids in order (i minus
 //         the retained before i) and the draw length;
 //      b. the drawn scores enter the ring in draw order (only the last `cap`
-//         of them can survive), and the ring state is advanced.
+//         of them can survive), and the ring state is advanced;
+//      c. given the offsets (the fused step), the compaction's block partials
+//         of the keep flags are written as well.
 #include "device_util.hpp"
 #include "kernels.hpp"
 #include "select_block.hpp"
