@@ -201,3 +201,28 @@ def test_stream_step_fused_shapes(pace, n):
         assert np.array_equal(H(bufs["offsets_out"])[: okept + 1], ooff)
         assert np.array_equal(H(bufs["kept_ids"])[:okept], oids)
         assert np.array_equal(H(bufs["cols_out"][0])[:nk], opacked[0])
+
+
+def test_stream_admit_unaligned_scores(pace):
+    """A score array that is not 16-byte aligned takes the draw's element
+    loads; same results as the oracle across ragged pool sizes."""
+    rng = np.random.default_rng(77)
+    for n in (1, 511, 513, 4096, 8193):
+        s = rng.normal(5.0, 2.0, n).round(1)
+        big = torch.empty(n + 1, dtype=torch.float64, device=DEV)
+        big[1:] = D(s)
+        sv = big[1:]
+        assert sv.data_ptr() % 16 != 0
+        ow = oracle.StreamWindow(128)
+        gw = pace.StreamWindow(128, DEV)
+        B = int(rng.integers(1, n + 2))
+        for step in range(2):
+            say("stream admit unaligned n=%d step=%d B=%d" % (n, step, B))
+            params = pace.default_params(window_min=4)
+            st, keep, rej, kappa, counts = pace.pace_stream_admit(sv, 0.5, gw, B, params)
+            torch.cuda.synchronize()
+            ost, okappa, odrawn, okept = oracle.stream_admit(s, 0.5, ow, B, window_min=4)
+            assert np.array_equal(H(st), ost)
+            assert float(H(kappa)[0]) == okappa
+            assert list(H(counts)) == [odrawn, okept, odrawn - okept]
+            assert np.array_equal(H(gw.ring).view(np.uint64), ow.ring.view(np.uint64))
