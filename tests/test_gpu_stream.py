@@ -156,7 +156,7 @@ def test_stream_step_fused_matches_oracle(pace):
         assert np.array_equal(H(bufs["cols_out"][0])[:nk], opacked[0])
 
 
-@pytest.mark.parametrize("n", [1, 17, 1000, 8192, 8193, 9000])
+@pytest.mark.parametrize("n", [0, 1, 17, 1000, 8192, 8193, 9000])
 def test_stream_step_fused_shapes(pace, n):
     """pace_stream_step on ragged pools: partial 16-trajectory blocks and
     partial waves of the draw, empty and multi-piece (> 16384-token)
