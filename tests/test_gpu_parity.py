@@ -117,7 +117,7 @@ def test_pool_parity(pace, name, mode, fused):
 
 
 @FUSED
-@pytest.mark.parametrize("mode", ["effective", "raw"])
+@pytest.mark.parametrize("mode", ["effective", "raw", "gen"])
 def test_stress_pool_parity(pace, mode, fused):
     pool = poolgen.make_pool("stress")
     say("stress %s fused %s n=%d tokens=%d" % (mode, fused, pool.n, pool.n_tokens))
@@ -133,6 +133,18 @@ def test_other_seeds(pace, name, seed, fused):
     pool = poolgen.make_pool(name, seed=seed, n=512 if name != "tiny" else None)
     say("seed %d pool %s fused %s" % (seed, name, fused))
     assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), "%s seed %d" % (name, seed))
+
+
+@FUSED
+def test_stress_three_columns(pace, fused):
+    """The stress pool with the three payload columns the benchmark's
+    multi-column run carries: tags, int32 token ids, fp32 log-probs."""
+    pool = poolgen.make_pool("stress")
+    rng = np.random.default_rng(11)
+    N = pool.n_tokens
+    cols = [pool.tags, rng.integers(0, 150000, N).astype(np.int32), rng.standard_normal(N).astype(np.float32)]
+    say("stress three columns fused %s tokens=%d" % (fused, N))
+    assert_same(gpu_step(pace, pool, cols=cols, fused=fused), oracle_step(pool, cols=cols), "stress/3 cols")
 
 
 @FUSED
