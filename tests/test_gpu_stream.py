@@ -226,3 +226,45 @@ def test_stream_admit_unaligned_scores(pace):
             assert float(H(kappa)[0]) == okappa
             assert list(H(counts)) == [odrawn, okept, odrawn - okept]
             assert np.array_equal(H(gw.ring).view(np.uint64), ow.ring.view(np.uint64))
+
+
+def test_stream_sweep_stress_pool(pace):
+    """The benchmark's streaming sweep configuration on the full stress pool:
+    batch ceil(capacity / 3), a 512-entry window, beta 0.9, effective scores
+    with prefix scores; six sweep steps (5% of slots refreshed per step), every
+    output against the oracle's chain."""
+    pool = copy.deepcopy(poolgen.make_pool("stress"))
+    V0 = pool.V
+    B = -(-pool.capacity // 3)
+    ow = oracle.StreamWindow(512)
+    gw = pace.StreamWindow(512, DEV)
+    params = pace.default_params(beta=0.9)
+    rh_o = rh_g = 0.0
+    tags, off, comp, pre, win = D(pool.tags), D(pool.offsets), D(pool.completion), D(pool.prefix_score), D(pool.window)
+    bufs = None
+    for step in range(6):
+        slots = poolgen.sweep_step(pool, step, V0)
+        for i in slots:
+            lo, hi = int(pool.offsets[i]), int(pool.offsets[i + 1])
+            tags[lo:hi] = D(pool.tags[lo:hi])
+        comp.copy_(D(pool.completion))
+        pre.copy_(D(pool.prefix_score))
+        bufs, rh_g = pace.pace_stream_step(tags, off, comp, pool.V, pool.occupancy, pool.capacity, [tags], gw, B,
+                                           pre, win, params, rh_g, bufs)
+        torch.cuda.synchronize()
+        osc, _, _ = oracle.score(pool.tags, pool.offsets, pool.completion, pool.V, pool.prefix_score, pool.window)
+        _, rh_o = oracle.budget(pool.occupancy, pool.capacity, rh_o, 0.9, 0.9)
+        ost, okappa, odrawn, okept = oracle.stream_admit(osc, rh_o, ow, B, window_min=32)
+        ooff, oids, opacked = oracle.compact(pool.offsets, (ost == 1).astype(np.uint8), [pool.tags])
+        say("stream sweep stress step %d drawn=%d kept=%d kappa=%r" % (step, odrawn, okept, okappa))
+        assert rh_g == rh_o
+        assert np.array_equal(H(bufs["score"])[: pool.n].view(np.uint64), osc.view(np.uint64))
+        assert np.array_equal(H(bufs["status"])[: pool.n], ost)
+        assert float(H(bufs["kappa"])[0]) == okappa
+        assert list(H(bufs["counts"])) == [odrawn, okept, odrawn - okept]
+        assert np.array_equal(H(gw.ring).view(np.uint64), ow.ring.view(np.uint64))
+        nk = int(H(bufs["n_kept_tokens"])[0])
+        assert nk == int(ooff[-1])
+        assert np.array_equal(H(bufs["offsets_out"])[: okept + 1], ooff)
+        assert np.array_equal(H(bufs["kept_ids"])[:okept], oids)
+        assert np.array_equal(H(bufs["cols_out"][0])[:nk], opacked[0])
