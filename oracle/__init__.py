@@ -64,12 +64,28 @@ def load_library(path: str):
     return lib
 
 
+def build_sanitized(out_path: str) -> str:
+    """Compile a copy of the oracle with AddressSanitizer and
+    UndefinedBehaviorSanitizer (any finding aborts), for the sanitizer run of
+    the pin suite; returns its path."""
+    subprocess.check_call(["gcc", "-O1", "-g", "-std=c99", "-fPIC", "-shared",
+                           "-ffp-contract=off", "-fno-fast-math", "-fno-omit-frame-pointer",
+                           "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                           "-o", out_path, _SRC, "-lm"])
+    return out_path
+
+
 def _load():
+    """The oracle library: the in-tree build, or the build named by
+    PACE_ORACLE_LIB (the sanitizer run of the pin suite sets it)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
-            build(force=False)
-        _lib = load_library(_LIB_PATH)
+        path = os.environ.get("PACE_ORACLE_LIB")
+        if not path:
+            path = _LIB_PATH
+            if not os.path.exists(path):
+                build(force=False)
+        _lib = load_library(path)
     return _lib
 
 

@@ -65,13 +65,29 @@ int oracle_validate(const int32_t *tags, const int64_t *offsets, int64_t n,
     return ORC_OK;
 }
 
-/* Integer power for the exact form of phi_gamma. */
+/* Integer power for the exact form of phi_gamma (callers keep x^g < 2^53). */
 static int64_t ipow(int64_t x, int g)
 {
     int64_t r = 1;
     for (int k = 0; k < g; k++)
         r *= x;
     return r;
+}
+
+/* 1 when W^g < 2^53, so that every a^g and (W-a)^g with 0 <= a <= W, and
+ * their sum W^g at most, is an exact integer in a double; 0 otherwise. Each
+ * factor is tested against the bound before it is multiplied in, so no
+ * intermediate product can overflow. */
+static int window_power_fits(int64_t W, int g)
+{
+    const int64_t limit = ((int64_t)1 << 53) - 1;
+    int64_t r = 1;
+    for (int k = 0; k < g; k++) {
+        if (W != 0 && r > limit / W)
+            return 0;
+        r *= W;
+    }
+    return 1;
 }
 
 /* ------------------------------------------------------------------------
@@ -99,7 +115,7 @@ int oracle_score(const int32_t *tags, const int64_t *offsets, int64_t n,
         !(w_wait >= 0.0) || isinf(w_wait) || (W > 0 && !window))
         return ORC_ERR_ARG;
     /* the exact form needs W^gamma representable in a double */
-    if (W > 0 && (double)ipow(W, gamma) >= 9007199254740992.0)
+    if (W > 0 && !window_power_fits(W, gamma))
         return ORC_ERR_ARG;
     int rc = oracle_validate(tags, offsets, n, n_tokens, completion, V);
     if (rc != ORC_OK)

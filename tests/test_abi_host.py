@@ -127,6 +127,36 @@ def test_score_host_argument_errors(L):
     assert call(wsb=16) == -2                   # too small
 
 
+def test_window_power_bound_matches_oracle(L):
+    """pace_score and the oracle accept and reject the same (window size,
+    gamma) pairs: the exact form of Eq. (9) needs W^gamma < 2^53. An accepted
+    pair gets as far as the workspace check (-2), a rejected one stops at the
+    argument check (-1); the oracle returns a score or its argument error."""
+    import paper_2609_36830_amd as pace
+    from tests.test_oracle_pins import WINDOW_POWER_BOUNDS, _score_rc
+    p = pace.default_params()
+
+    def gpu_rc(W, gamma):
+        p.gamma = gamma
+        return L.pace_score(FAKE, FAKE, 1, 1, FAKE, 5, None, FAKE, W, ctypes.byref(p), FAKE, None, None,
+                            FAKE, 0, None)
+
+    grid = []
+    for gam, Wmax in WINDOW_POWER_BOUNDS.items():
+        grid += [(Wmax - 1, gam), (Wmax, gam), (Wmax + 1, gam), (Wmax + 2, gam)]
+    grid += [(W, 4) for W in (1, 512, 4096, 55108, 55109, 55110, 65536)]
+    grid += [(W, g) for g in (1, 2, 3) for W in (1, 512, 65536)]
+    for W, gam in grid:
+        ref = _score_rc(W, gam)
+        accepted = not isinstance(ref, int)
+        assert accepted or ref == oracle.ERR_ARG
+        assert gpu_rc(W, gam) == (-2 if accepted else -1), (W, gam)
+    # sizes no host array can hold: only the library's check is exercised
+    for W, gam, acc in ((2 ** 53 - 1, 1, True), (2 ** 53, 1, False), (2 ** 40, 4, False), (2 ** 62, 2, False),
+                        (2 ** 31, 3, False)):
+        assert gpu_rc(W, gam) == (-2 if acc else -1), (W, gam)
+
+
 def test_filter_step_host_argument_errors(L):
     """pace_filter_step rejects bad arguments before enqueuing, r_hat untouched."""
     import paper_2609_36830_amd as pace

@@ -85,6 +85,11 @@ MUTATIONS = [
     ("diagnostics K_gen over all tokens", "m[1] = (T > 0) ? (double)S / (double)T : 0.0;",
      "m[1] = (T > 0) ? (double)S / (double)(offsets[i + 1] - offsets[i]) : 0.0;"),
     ("diagnostics totals miss T", "tot[3] += T;", "tot[3] += S;"),
+    ("window power guard removed", "if (W > 0 && !window_power_fits(W, gamma))", "if (0)"),
+    ("window power guard computed without overflow check", "if (W > 0 && !window_power_fits(W, gamma))",
+     "if (W > 0 && (double)ipow(W, gamma) >= 9007199254740992.0)"),
+    ("window power guard takes one factor too many", "for (int k = 0; k < g; k++) {\n        if (W != 0",
+     "for (int k = 0; k <= g; k++) {\n        if (W != 0"),
     ("stream window misses the newest entry", "sorted[t] = ring[(head - cnt + t + cap) % cap];",
      "sorted[t] = ring[(head - cnt + t + cap - 1) % cap];"),
 ]

@@ -187,6 +187,51 @@ def test_missing_prefix_or_short_window_gives_full_penalty():
     assert _F_via_gen_only(float("nan"), np.arange(1, 600, dtype=float), 4, window_min=32) == 1.0
 
 
+# Largest window W with W^gamma < 2^53 for each integer gamma (worked out by
+# hand: 94906265^2 = 9007199136250225, 208063^3 = 9007091372906047 and
+# 9741^4 = 9003558140700561 lie below 2^53 = 9007199254740992; the next W
+# does not). Up to that size every a^gamma, (W - a)^gamma and their sum is an
+# exact integer in binary64, so Eq. (9) is one correctly rounded division.
+WINDOW_POWER_BOUNDS = {2: 94906265, 3: 208063, 4: 9741}
+
+
+def _score_rc(W, gamma, prefix=None):
+    """Return code of oracle.score on a one-trajectory pool with a window of
+    W equal entries (sorted); the zero-filled window costs no memory until
+    read."""
+    return oracle.score(np.array([4], np.int32), np.array([0, 1], np.int64), np.array([5], np.int32), 5,
+                        prefix=prefix, window=np.zeros(W), w_wait=0.0, gamma=gamma, window_min=1, check=False)
+
+
+def test_window_power_bound_per_gamma():
+    """The exact form of Eq. (9) needs W^gamma < 2^53: the oracle accepts the
+    largest such W for every gamma and rejects the next one, without the
+    power overflowing on the way."""
+    for gam, W in WINDOW_POWER_BOUNDS.items():
+        ok = _score_rc(W, gam)
+        assert not isinstance(ok, int), (gam, W, ok)
+        assert _score_rc(W + 1, gam) == oracle.ERR_ARG, (gam, W + 1)
+    # gamma = 4 past the point where W^4 no longer fits in 63 bits (55109^4 >
+    # 2^63): a power computed without a check would wrap and pass the test
+    for W in (55108, 55109, 55110, 65536, 100000):
+        assert _score_rc(W, 4) == oracle.ERR_ARG, W
+    assert not isinstance(_score_rc(4096, 4), int)
+
+
+def test_phi_exact_at_the_largest_window():
+    """At W = 9741, gamma = 4 (the largest window for gamma 4), F is the
+    correctly rounded q^4 / (q^4 + (1-q)^4) of Eq. (9) and lies in [0, 1]
+    (Eq. (7)); s runs over ranks 0, 1, W/2, W-1 and W."""
+    W = WINDOW_POWER_BOUNDS[4]
+    window = np.arange(1, W + 1, dtype=float)
+    for a in (0, 1, W // 2, W // 2 + 1, W - 1, W):
+        F = _F_via_gen_only(float(a) + 0.5, window, 4)
+        q = Fraction(a, W)
+        exact = q ** 4 / (q ** 4 + (1 - q) ** 4)
+        assert F == float(exact), (a, F, float(exact))
+        assert 0.0 <= F <= 1.0
+
+
 def test_effective_and_gen_only_variants():
     """Eq. (7): K_eff = K_wait + F K_gen; generation-only variant: w_wait = 0."""
     rng = np.random.default_rng(5)
