@@ -36,6 +36,9 @@
  * - A failed kernel launch returns PACE_ERR_HIP.
  * - Every result is a deterministic function of the inputs: identical bits
  *   run to run and for any stream.
+ * - No call keeps state from one call to the next, apart from the per-thread
+ *   timers that the measurement hook pace_time_next_kernel arms for the
+ *   following device call only.
  * - Workspace: at least pace_workspace_bytes() bytes, 256-byte aligned. Its
  *   contents need no initialisation and are scratch between calls; calls
  *   sharing one workspace must be ordered (same stream).
@@ -359,11 +362,18 @@ int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t 
                      const double *edges, int nbins, int64_t *hist_out, int64_t *totals_out, void *stream);
 
 /* pace_time_next_kernel -- measurement hook, not part of the method.
- * Arms a one-shot timer for one phase of the device work on the calling host
- * thread: the next kernel of that phase launched from this thread (by any
- * entry point, on any stream) is launched with hipExtLaunchKernel and the two
- * events, so that hipEventElapsedTime(start, stop) afterwards gives that
- * kernel's own execution time. The launch consumes the timer.
+ * Arms a one-shot timer for one phase of the device work of the NEXT call
+ * made from the calling host thread to an entry point that enqueues device
+ * work (every call above except pace_default_params, pace_workspace_bytes,
+ * pace_budget and pace_strerror): that call launches its first kernel of the
+ * phase with hipExtLaunchKernel and the two events, so that
+ * hipEventElapsedTime(start, stop) afterwards gives that kernel's own
+ * execution time. When that call returns, every timer armed on the thread is
+ * dropped, used or not: a timer never reaches a later call.
+ * The armed timers are the library's only state between calls: a per-thread
+ * table of at most PACE_PHASE_COUNT event pairs, empty except between
+ * pace_time_next_kernel and the return of the next device call on that
+ * thread. Calls on other threads never see it.
  * phase: PACE_PHASE_REDUCE (token reduction of pace_score), PACE_PHASE_FINALIZE
  *   (score finalisation), PACE_PHASE_SELECT (the rank kernel, the
  *   single-workgroup select of large pools, or the streaming draw),

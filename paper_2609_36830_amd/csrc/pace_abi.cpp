@@ -71,6 +71,20 @@ bool take_phase_timer(int phase, hipEvent_t *start, hipEvent_t *stop) {
     return true;
 }
 
+namespace {
+// Every entry point that enqueues device work holds one of these: when the
+// call returns, the thread's armed timers are dropped, used or not, so a
+// timer never reaches a later call.
+struct TimerScope {
+    TimerScope() = default;
+    TimerScope(const TimerScope &) = delete;
+    TimerScope &operator=(const TimerScope &) = delete;
+    ~TimerScope() {
+        for (int k = 0; k < kPhaseCount; ++k) g_phase_timer[k][0] = g_phase_timer[k][1] = nullptr;
+    }
+};
+}  // namespace
+
 }  // namespace pace
 
 extern "C" {
@@ -162,6 +176,7 @@ int pace_score(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int6
                const double *window_sorted, int64_t window_n, const pace_params *params,
                double *score_out, int64_t *gen_sum_out, int64_t *gen_count_out, void *workspace,
                size_t workspace_bytes, void *stream) {
+    const TimerScope timers;
     const pace_params p = params_or_default(params);
     int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
                               prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
@@ -178,8 +193,8 @@ int pace_score(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int6
                                    aligned(tags, 16), (hipStream_t)stream));
 }
 
-int pace_budget(int64_t occupancy, int64_t capacity, const pace_params *params,
-                double *r_hat_inout, int64_t *budget_out) {
+static int budget_impl(int64_t occupancy, int64_t capacity, const pace_params *params,
+                       double *r_hat_inout, int64_t *budget_out) {
     const pace_params p = params_or_default(params);
     if (!r_hat_inout || !budget_out || occupancy < 0 || capacity < 0) return PACE_ERR_INVALID_ARG;
     if (!(p.beta >= 0.0 && p.beta < 1.0) || !(p.r_max >= 0.0 && p.r_max <= 1.0))
@@ -206,8 +221,14 @@ int pace_budget(int64_t occupancy, int64_t capacity, const pace_params *params,
     return PACE_OK;
 }
 
+int pace_budget(int64_t occupancy, int64_t capacity, const pace_params *params,
+                double *r_hat_inout, int64_t *budget_out) {
+    return budget_impl(occupancy, capacity, params, r_hat_inout, budget_out);
+}
+
 int pace_select(const double *score, int64_t n_traj, int64_t budget, uint8_t *keep_out,
                 int32_t *reject_ids_out, void *workspace, size_t workspace_bytes, void *stream) {
+    const TimerScope timers;
     if (n_traj < 0 || n_traj >= INT32_MAX || budget < 0 || budget > n_traj) return PACE_ERR_INVALID_ARG;
     if (n_traj > 0 && (!score || !keep_out)) return PACE_ERR_INVALID_ARG;
     if (budget > 0 && !reject_ids_out) return PACE_ERR_INVALID_ARG;
@@ -223,6 +244,7 @@ int pace_compact(const int64_t *offsets, int64_t n_traj, int64_t n_tokens, const
                  void *const *cols_out, int64_t *offsets_out, int32_t *kept_ids_out,
                  int64_t *n_kept_tokens_out, void *workspace, size_t workspace_bytes,
                  void *stream) {
+    const TimerScope timers;
     CompactCols cols;
     int rc = check_compact_args(offsets, n_traj, n_tokens, keep, n_cols, cols_in, elem_bytes, cols_out,
                                 offsets_out, kept_ids_out, n_kept_tokens_out, &cols);
@@ -243,6 +265,7 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
                      const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
                      int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
                      size_t workspace_bytes, void *stream) {
+    const TimerScope timers;
     const pace_params p = params_or_default(params);
     int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
                               prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
@@ -258,7 +281,7 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
         return PACE_ERR_WORKSPACE;
     double r_hat = *r_hat_inout;
     int64_t budget = 0;
-    rc = pace_budget(occupancy, capacity, &p, &r_hat, &budget);
+    rc = budget_impl(occupancy, capacity, &p, &r_hat, &budget);
     if (rc != PACE_OK) return rc;
     if (budget > n_traj || (budget > 0 && !reject_ids_out)) return PACE_ERR_INVALID_ARG;
     const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
@@ -283,6 +306,7 @@ static int check_groups_arg(const int64_t *group_offsets, int64_t n_groups) {
 
 int pace_group_score(const double *score, int64_t n_traj, const int64_t *group_offsets, int64_t n_groups,
                      double *group_score_out, void *stream) {
+    const TimerScope timers;
     if (n_traj < 0 || n_traj >= INT32_MAX || check_groups_arg(group_offsets, n_groups) != PACE_OK)
         return PACE_ERR_INVALID_ARG;
     if ((n_traj > 0 && !score) || (n_groups > 0 && !group_score_out) || !aligned(score, 8) ||
@@ -294,6 +318,7 @@ int pace_group_score(const double *score, int64_t n_traj, const int64_t *group_o
 
 int pace_group_expand(const int64_t *group_offsets, int64_t n_groups, int64_t n_traj,
                       const uint8_t *group_keep, uint8_t *keep_out, void *stream) {
+    const TimerScope timers;
     if (n_traj < 0 || n_traj >= INT32_MAX || check_groups_arg(group_offsets, n_groups) != PACE_OK)
         return PACE_ERR_INVALID_ARG;
     if ((n_groups > 0 && !group_keep) || (n_traj > 0 && !keep_out)) return PACE_ERR_INVALID_ARG;
@@ -303,6 +328,7 @@ int pace_group_expand(const int64_t *group_offsets, int64_t n_groups, int64_t n_
 
 int pace_validate_groups(const int64_t *group_offsets, int64_t n_groups, int64_t n_traj,
                          int32_t *err_word_out, void *stream) {
+    const TimerScope timers;
     if (n_traj < 0 || n_traj >= INT32_MAX || check_groups_arg(group_offsets, n_groups) != PACE_OK)
         return PACE_ERR_INVALID_ARG;
     if (!err_word_out || !aligned(err_word_out, 4)) return PACE_ERR_INVALID_ARG;
@@ -321,6 +347,7 @@ int pace_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t 
                            const void *const *cols_in, const int32_t *elem_bytes, void *const *cols_out,
                            int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
                            void *workspace, size_t workspace_bytes, void *stream) {
+    const TimerScope timers;
     const pace_params p = params_or_default(params);
     int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
                               prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
@@ -339,7 +366,7 @@ int pace_group_filter_step(const int32_t *tags, const int64_t *offsets, int64_t 
         return PACE_ERR_WORKSPACE;
     double r_hat = *r_hat_inout;
     int64_t budget = 0;
-    rc = pace_budget(occupancy, capacity, &p, &r_hat, &budget);
+    rc = budget_impl(occupancy, capacity, &p, &r_hat, &budget);
     if (rc != PACE_OK) return rc;
     if (budget > n_groups || (budget > 0 && !reject_group_ids_out)) return PACE_ERR_INVALID_ARG;
     const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
@@ -359,6 +386,7 @@ int pace_stream_admit(const double *score, int64_t n_traj, double r_hat, const p
                       int64_t batch_size, double *window_ring, int64_t window_cap, int64_t *window_state,
                       uint8_t *status_out, uint8_t *keep_out, int32_t *reject_ids_out, double *kappa_out,
                       int64_t *counts_out, void *stream) {
+    const TimerScope timers;
     const pace_params p = params_or_default(params);
     if (n_traj < 0 || n_traj >= INT32_MAX || batch_size < 0) return PACE_ERR_INVALID_ARG;
     if (!(r_hat >= 0.0) || isinf(r_hat) || !(p.r_max >= 0.0 && p.r_max <= 1.0) || p.window_min < 0)
@@ -386,6 +414,7 @@ int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
                      const void *const *cols_in, const int32_t *elem_bytes, void *const *cols_out,
                      int64_t *offsets_out, int32_t *kept_ids_out, int64_t *n_kept_tokens_out,
                      void *workspace, size_t workspace_bytes, void *stream) {
+    const TimerScope timers;
     const pace_params p = params_or_default(params);
     int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
                               prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
@@ -406,7 +435,7 @@ int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
         return PACE_ERR_WORKSPACE;
     double r_hat = *r_hat_inout;
     int64_t budget = 0;
-    rc = pace_budget(occupancy, capacity, &p, &r_hat, &budget);
+    rc = budget_impl(occupancy, capacity, &p, &r_hat, &budget);
     if (rc != PACE_OK) return rc;
     const int64_t wmin = p.window_min > 1 ? p.window_min : 1;
     const bool use_prefix = prefix_score != nullptr && window_n >= wmin;
@@ -445,6 +474,7 @@ int pace_stream_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
 int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32_t *tags,
                       const int64_t *prefix_offsets, int64_t n, int64_t n_tokens, int64_t cap,
                       int64_t min_tokens, double *s_pre_out, void *stream) {
+    const TimerScope timers;
     if (n < 0 || n >= INT32_MAX || n_tokens < 0 || cap < 0 || min_tokens < 0 || !prefix_offsets)
         return PACE_ERR_INVALID_ARG;
     if ((n > 0 && !s_pre_out) || (n_tokens > 0 && (!lp_new || !lp_behavior))) return PACE_ERR_INVALID_ARG;
@@ -458,6 +488,7 @@ int pace_prefix_score(const float *lp_new, const float *lp_behavior, const int32
 int pace_stale_k(const int64_t *gen_sum, const int64_t *gen_count, const int32_t *completion,
                  int32_t current_version, int64_t n_traj, int64_t k, uint8_t *keep_out, double *lag_out,
                  void *stream) {
+    const TimerScope timers;
     if (n_traj < 0 || n_traj >= INT32_MAX || k < 0 || k >= INT32_MAX || current_version < 0)
         return PACE_ERR_INVALID_ARG;
     if (n_traj > 0 && (!gen_sum || !gen_count || !completion || !keep_out)) return PACE_ERR_INVALID_ARG;
@@ -470,6 +501,7 @@ int pace_stale_k(const int64_t *gen_sum, const int64_t *gen_count, const int32_t
 int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t *gen_count,
                      const int32_t *completion, int32_t current_version, const uint8_t *keep, int64_t n_traj,
                      const double *edges, int nbins, int64_t *hist_out, int64_t *totals_out, void *stream) {
+    const TimerScope timers;
     if (n_traj < 0 || n_traj >= INT32_MAX || nbins < 1 || nbins > kDiagBinsMax || current_version < 0)
         return PACE_ERR_INVALID_ARG;
     if (!edges || !hist_out || !totals_out) return PACE_ERR_INVALID_ARG;
@@ -494,6 +526,7 @@ int pace_time_next_kernel(int phase, void *start_event, void *stop_event) {
 int pace_validate(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
                   const int32_t *completion, int32_t current_version, const double *window_sorted,
                   int64_t window_n, int32_t *err_word_out, void *stream) {
+    const TimerScope timers;
     if (n_traj < 0 || n_traj >= INT32_MAX || n_tokens < 0 || window_n < 0) return PACE_ERR_INVALID_ARG;
     if (!offsets || !err_word_out || (n_traj > 0 && !completion) || (n_tokens > 0 && !tags) ||
         (window_n > 0 && !window_sorted))

@@ -1,0 +1,79 @@
+"""The measurement hook pace_time_next_kernel only reaches the next device
+call made from the same thread: a timer armed for a phase that call does not
+run is dropped when the call returns, so it never attaches to a later,
+unrelated kernel."""
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def say(msg):
+    sys.stdout.write("[gpu] %s\n" % msg)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def pace():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import os
+    from paper_2609_36830_amd import _lib
+    if not os.path.exists(_lib.library_path):
+        from paper_2609_36830_amd import build
+        build.build()
+    import paper_2609_36830_amd as pace
+    return pace
+
+
+def _pool(n=4096, length=16384):
+    """n trajectories of `length` single-version tokens, every one kept: the
+    compaction copies n * length int32 tags (268 MB), long enough (tens of
+    microseconds) to tell a timed kernel from two back-to-back events."""
+    off = torch.arange(0, (n + 1) * length, length, dtype=torch.int64, device=DEV)
+    tags = torch.full((n * length,), 3, dtype=torch.int32, device=DEV)
+    comp = torch.full((n,), 3, dtype=torch.int32, device=DEV)
+    keep = torch.ones(n, dtype=torch.uint8, device=DEV)
+    return off, tags, comp, keep
+
+
+def _events():
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    b.record()
+    torch.cuda.synchronize()
+    return a, b
+
+
+def test_unused_timer_is_dropped_when_the_call_returns(pace):
+    off, tags, comp, keep = _pool()
+    say("timer scope: pace_score with the compaction phase armed, then pace_compact")
+    a, b = _events()
+    before = a.elapsed_time(b)
+    pace.pace_time_next_kernel(pace.PHASE_COMPACT, a, b)
+    pace.pace_score(tags, off, comp, 5)                        # no compaction kernel in this call
+    out = pace.pace_compact(off, keep, [tags])
+    torch.cuda.synchronize()
+    assert a.elapsed_time(b) == before                        # the events were not recorded again
+    assert int(out[2].item()) == tags.numel()
+
+
+def test_timer_reaches_the_next_device_call(pace):
+    off, tags, comp, keep = _pool()
+    say("timer scope: compaction phase armed, pace_budget (host only), then pace_compact")
+    a, b = _events()
+    before = a.elapsed_time(b)
+    pace.pace_time_next_kernel(pace.PHASE_COMPACT, a, b)
+    pace.pace_budget(10, 5)                                   # host-only calls leave the timer armed
+    pace.pace_compact(off, keep, [tags])
+    torch.cuda.synchronize()
+    t = a.elapsed_time(b)
+    assert t != before and t > 0.02                           # the copy of 268 MB takes over 20 us
+    # consumed: a second compaction leaves the events alone
+    pace.pace_compact(off, keep, [tags])
+    torch.cuda.synchronize()
+    assert a.elapsed_time(b) == t
