@@ -58,6 +58,7 @@ extern "C" {
 #define PACE_ERR_WORKSPACE (-2)
 #define PACE_ERR_PRECONDITION (-3)
 #define PACE_ERR_HIP (-4)
+#define PACE_ERR_SCRATCH_LIMIT (-5) /* pace_filter_step_noalloc: pool beyond the fixed scratch */
 
 /* Bits of the device error word written by pace_validate. */
 #define PACE_BAD_OFFSETS 0x1    /* offsets[0] != 0, decreasing, or offsets[n] != n_tokens */
@@ -209,6 +210,33 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
                      const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
                      int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
                      size_t workspace_bytes, void *stream);
+
+/* pace_filter_step_noalloc -- pace_filter_step for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the same arguments, results and kernels,
+ * with no workspace argument. The workspace is instead a fixed array of
+ * PACE_NOALLOC_SCRATCH_BYTES bytes in device memory, one per device, which the
+ * library holds from its load until the process ends; the call allocates and
+ * frees nothing. The array of the device current on the calling thread is
+ * used, so `stream` must belong to that device.
+ * Limit: the pool's workspace, pace_workspace_bytes(PACE_WS_FILTER_STEP,
+ * n_traj, n_tokens), must fit in the array (for example 4096 trajectories of
+ * up to ~1.8e9 tokens, or 65536 trajectories of up to ~1.6e9 tokens); a larger
+ * pool returns PACE_ERR_SCRATCH_LIMIT after the argument checks, before
+ * anything is enqueued.
+ * Every call on one device shares that device's array: calls that may overlap
+ * on one device (different streams, or threads) race and must be ordered by
+ * the caller. No call relies on what an earlier call left in the array. */
+#define PACE_NOALLOC_SCRATCH_BYTES (16u << 20)
+int pace_filter_step_noalloc(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                             const int32_t *completion, int32_t current_version,
+                             const double *prefix_score, const double *window_sorted, int64_t window_n,
+                             int64_t occupancy, int64_t capacity, const pace_params *params,
+                             double *r_hat_inout, int64_t *budget_out, double *score_out,
+                             int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *keep_out,
+                             int32_t *reject_ids_out, int n_cols, const void *const *cols_in,
+                             const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
+                             int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *stream);
 
 /* ---- Group-level admission (Appendix B) ------------------------------------
  * The full method aggregates by the mean within prompt groups; its score

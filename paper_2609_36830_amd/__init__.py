@@ -24,7 +24,8 @@ from ._lib import PaceParams, lib, library_path
 
 __all__ = [
     "PaceError", "PaceParams", "default_params", "pace_workspace_bytes", "pace_score",
-    "pace_budget", "pace_select", "pace_compact", "pace_validate", "pace_filter_step", "FilterStep",
+    "pace_budget", "pace_select", "pace_compact", "pace_validate", "pace_filter_step",
+    "pace_filter_step_noalloc", "FilterStep",
     "library_path", "WS_SCORE", "WS_SELECT", "WS_COMPACT", "WS_FILTER_STEP",
     "BAD_OFFSETS", "BAD_COMPLETION", "BAD_TAG", "BAD_WINDOW",
 ]
@@ -206,7 +207,7 @@ def pace_filter_step(tags, offsets, completion, current_version, occupancy, capa
                      r_hat_prev: float = 0.0, score_out=None, gen_sum_out=None, gen_count_out=None,
                      keep_out=None, reject_ids_out=None, cols_out=None, offsets_out=None,
                      kept_ids_out=None, n_kept_tokens_out=None, workspace=None, stream=None,
-                     with_counts=True):
+                     with_counts=True, _noalloc=False):
     """One whole filter step (Algorithm 1). Returns a dict with budget, r_hat and
     the outputs of pace_score / pace_select / pace_compact (full-capacity tensors;
     reject_ids is cut to the budget)."""
@@ -237,24 +238,41 @@ def pace_filter_step(tags, offsets, completion, current_version, occupancy, capa
     offsets_out = e(n + 1, torch.int64) if offsets_out is None else offsets_out
     kept_ids_out = e(max(n, 1), torch.int32) if kept_ids_out is None else kept_ids_out
     n_kept_tokens_out = e(1, torch.int64) if n_kept_tokens_out is None else n_kept_tokens_out
-    ws = _workspace(WS_FILTER_STEP, n, nt, dev, workspace)
     nc = len(cols)
     cin = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols])
     cout = (ctypes.c_void_p * max(nc, 1))(*[c.data_ptr() for c in cols_out])
     eb = (ctypes.c_int32 * max(nc, 1))(*[c.element_size() for c in cols])
     rh = ctypes.c_double(float(r_hat_prev))
     b = ctypes.c_int64(0)
-    _check(lib().pace_filter_step(_ptr(tags), _ptr(offsets), n, nt, _ptr(completion), int(current_version),
-                                  _ptr(prefix_score), _ptr(window_sorted), W, int(occupancy), int(capacity),
-                                  ctypes.byref(params) if params is not None else None,
-                                  ctypes.byref(rh), ctypes.byref(b), _ptr(score_out), _ptr(gen_sum_out),
-                                  _ptr(gen_count_out), _ptr(keep_out), _ptr(reject_ids_out), nc, cin, eb,
-                                  cout, _ptr(offsets_out), _ptr(kept_ids_out), _ptr(n_kept_tokens_out),
-                                  _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_filter_step")
+    args = (_ptr(tags), _ptr(offsets), n, nt, _ptr(completion), int(current_version),
+            _ptr(prefix_score), _ptr(window_sorted), W, int(occupancy), int(capacity),
+            ctypes.byref(params) if params is not None else None,
+            ctypes.byref(rh), ctypes.byref(b), _ptr(score_out), _ptr(gen_sum_out),
+            _ptr(gen_count_out), _ptr(keep_out), _ptr(reject_ids_out), nc, cin, eb,
+            cout, _ptr(offsets_out), _ptr(kept_ids_out), _ptr(n_kept_tokens_out))
+    if _noalloc:
+        _check(lib().pace_filter_step_noalloc(*args, _stream(dev, stream)), "pace_filter_step_noalloc")
+    else:
+        ws = _workspace(WS_FILTER_STEP, n, nt, dev, workspace)
+        _check(lib().pace_filter_step(*args, _ptr(ws), ws.numel(), _stream(dev, stream)), "pace_filter_step")
     return dict(budget=int(b.value), r_hat=float(rh.value), score=score_out, gen_sum=gen_sum_out,
                 gen_count=gen_count_out, keep=keep_out, reject_ids=reject_ids_out[: int(b.value)],
                 offsets_out=offsets_out, kept_ids=kept_ids_out, n_kept_tokens=n_kept_tokens_out,
                 cols_out=cols_out)
+
+
+def pace_filter_step_noalloc(tags, offsets, completion, current_version, occupancy, capacity, cols, **kw):
+    """pace_filter_step with the workspace in the library's fixed device
+    scratch (PACE_NOALLOC_SCRATCH_BYTES per device): same arguments (no
+    `workspace`) and results. Allocates nothing when every output is passed."""
+    if "workspace" in kw:
+        raise ValueError("pace_filter_step_noalloc takes no workspace")
+    return pace_filter_step(tags, offsets, completion, current_version, occupancy, capacity, cols,
+                            _noalloc=True, **kw)
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20
+ERR_SCRATCH_LIMIT = -5
 
 
 def pace_group_score(score, group_offsets, group_score_out=None, stream=None):

@@ -28,6 +28,8 @@ SIGNATURES = [
     ("pace_validate", ctypes.c_int, [P, P, i64, i64, P, i32, P, i64, P, P]),
     ("pace_filter_step", ctypes.c_int, [P, P, i64, i64, P, i32, P, P, i64, i64, i64, P, P, P, P, P, P,
                                         P, P, ctypes.c_int, P, P, P, P, P, P, P, sz, P]),
+    ("pace_filter_step_noalloc", ctypes.c_int, [P, P, i64, i64, P, i32, P, P, i64, i64, i64, P, P, P, P, P,
+                                                P, P, P, ctypes.c_int, P, P, P, P, P, P, P]),
     ("pace_group_score", ctypes.c_int, [P, i64, P, i64, P, P]),
     ("pace_group_expand", ctypes.c_int, [P, i64, i64, P, P, P]),
     ("pace_validate_groups", ctypes.c_int, [P, i64, i64, P, P]),

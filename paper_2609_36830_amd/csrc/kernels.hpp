@@ -213,6 +213,11 @@ hipError_t launch_validate(const int32_t *tags, const int64_t *offsets, int64_t 
                            const int32_t *completion, int32_t V, const double *window, int64_t W,
                            int32_t *err_word, hipStream_t stream);
 
+// Device address of the current device's fixed scratch array
+// (PACE_NOALLOC_SCRATCH_BYTES bytes, 256-byte aligned), looked up once per
+// device.
+hipError_t noalloc_scratch(void **out);
+
 inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 }  // namespace pace

@@ -105,6 +105,7 @@ const char *pace_strerror(int code) {
         case PACE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
         case PACE_ERR_PRECONDITION: return "data precondition violated";
         case PACE_ERR_HIP: return "HIP launch failure";
+        case PACE_ERR_SCRATCH_LIMIT: return "pool too large for the fixed device scratch";
         default: return "unknown error code";
     }
 }
@@ -255,17 +256,20 @@ int pace_compact(const int64_t *offsets, int64_t n_traj, int64_t n_tokens, const
                                      kept_ids_out, n_kept_tokens_out, workspace, (hipStream_t)stream));
 }
 
-int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
-                     const int32_t *completion, int32_t current_version,
-                     const double *prefix_score, const double *window_sorted, int64_t window_n,
-                     int64_t occupancy, int64_t capacity, const pace_params *params,
-                     double *r_hat_inout, int64_t *budget_out, double *score_out,
-                     int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *keep_out,
-                     int32_t *reject_ids_out, int n_cols, const void *const *cols_in,
-                     const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
-                     int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
-                     size_t workspace_bytes, void *stream) {
-    const TimerScope timers;
+// pace_filter_step's checks and launches. With scratch_limit set, the
+// workspace is the fixed device scratch: a pool whose workspace exceeds it is
+// refused with PACE_ERR_SCRATCH_LIMIT after the argument checks, and
+// `workspace` is looked up only then.
+static int filter_step_impl(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                            const int32_t *completion, int32_t current_version,
+                            const double *prefix_score, const double *window_sorted, int64_t window_n,
+                            int64_t occupancy, int64_t capacity, const pace_params *params,
+                            double *r_hat_inout, int64_t *budget_out, double *score_out,
+                            int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *keep_out,
+                            int32_t *reject_ids_out, int n_cols, const void *const *cols_in,
+                            const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
+                            int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
+                            size_t workspace_bytes, bool scratch_limit, void *stream) {
     const pace_params p = params_or_default(params);
     int rc = check_score_args(tags, offsets, n_traj, n_tokens, completion, current_version,
                               prefix_score, window_sorted, window_n, p, score_out, gen_sum_out,
@@ -277,6 +281,12 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
     if (rc != PACE_OK) return rc;
     if (n_traj > 0 && !keep_out) return PACE_ERR_INVALID_ARG;
     if (!r_hat_inout || !budget_out || !aligned(reject_ids_out, 4)) return PACE_ERR_INVALID_ARG;
+    if (scratch_limit) {
+        if (filter_step_ws_bytes(n_traj, n_tokens) > (size_t)PACE_NOALLOC_SCRATCH_BYTES)
+            return PACE_ERR_SCRATCH_LIMIT;
+        if (noalloc_scratch(&workspace) != hipSuccess) return PACE_ERR_HIP;
+        workspace_bytes = PACE_NOALLOC_SCRATCH_BYTES;
+    }
     if (!workspace || !aligned(workspace, 256) || workspace_bytes < filter_step_ws_bytes(n_traj, n_tokens))
         return PACE_ERR_WORKSPACE;
     double r_hat = *r_hat_inout;
@@ -296,6 +306,41 @@ int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj
     *r_hat_inout = r_hat;
     *budget_out = budget;
     return PACE_OK;
+}
+
+int pace_filter_step(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                     const int32_t *completion, int32_t current_version,
+                     const double *prefix_score, const double *window_sorted, int64_t window_n,
+                     int64_t occupancy, int64_t capacity, const pace_params *params,
+                     double *r_hat_inout, int64_t *budget_out, double *score_out,
+                     int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *keep_out,
+                     int32_t *reject_ids_out, int n_cols, const void *const *cols_in,
+                     const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
+                     int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *workspace,
+                     size_t workspace_bytes, void *stream) {
+    const TimerScope timers;
+    return filter_step_impl(tags, offsets, n_traj, n_tokens, completion, current_version, prefix_score,
+                            window_sorted, window_n, occupancy, capacity, params, r_hat_inout, budget_out,
+                            score_out, gen_sum_out, gen_count_out, keep_out, reject_ids_out, n_cols, cols_in,
+                            elem_bytes, cols_out, offsets_out, kept_ids_out, n_kept_tokens_out, workspace,
+                            workspace_bytes, false, stream);
+}
+
+int pace_filter_step_noalloc(const int32_t *tags, const int64_t *offsets, int64_t n_traj, int64_t n_tokens,
+                             const int32_t *completion, int32_t current_version,
+                             const double *prefix_score, const double *window_sorted, int64_t window_n,
+                             int64_t occupancy, int64_t capacity, const pace_params *params,
+                             double *r_hat_inout, int64_t *budget_out, double *score_out,
+                             int64_t *gen_sum_out, int64_t *gen_count_out, uint8_t *keep_out,
+                             int32_t *reject_ids_out, int n_cols, const void *const *cols_in,
+                             const int32_t *elem_bytes, void *const *cols_out, int64_t *offsets_out,
+                             int32_t *kept_ids_out, int64_t *n_kept_tokens_out, void *stream) {
+    const TimerScope timers;
+    return filter_step_impl(tags, offsets, n_traj, n_tokens, completion, current_version, prefix_score,
+                            window_sorted, window_n, occupancy, capacity, params, r_hat_inout, budget_out,
+                            score_out, gen_sum_out, gen_count_out, keep_out, reject_ids_out, n_cols, cols_in,
+                            elem_bytes, cols_out, offsets_out, kept_ids_out, n_kept_tokens_out, nullptr, 0,
+                            true, stream);
 }
 
 static int check_groups_arg(const int64_t *group_offsets, int64_t n_groups) {

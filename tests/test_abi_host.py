@@ -182,6 +182,28 @@ def test_filter_step_host_argument_errors(L):
     assert rh.value == 0.25 and b.value == -7
 
 
+def test_filter_step_noalloc_limit(L):
+    """The scratch variant refuses a pool whose workspace exceeds its fixed
+    array, after the argument checks and before any launch."""
+    import paper_2609_36830_amd as pace
+    rh = ctypes.c_double(0.0)
+    b = ctypes.c_int64(0)
+    cols = (ctypes.c_void_p * 1)(FAKE)
+    e4 = (ctypes.c_int32 * 1)(4)
+
+    def call(n, nt, keep=FAKE):
+        return L.pace_filter_step_noalloc(FAKE, FAKE, n, nt, FAKE, 10, None, None, 0, 10, 5, None,
+                                          ctypes.byref(rh), ctypes.byref(b), FAKE, None, None, keep, FAKE, 1,
+                                          cols, e4, cols, FAKE, FAKE, FAKE, None)
+
+    assert pace.pace_workspace_bytes(3, 1 << 22, 1000) > pace.NOALLOC_SCRATCH_BYTES
+    assert call(1 << 22, 1000) == pace.ERR_SCRATCH_LIMIT
+    assert pace.pace_workspace_bytes(3, 4096, 4 * 10 ** 9) > pace.NOALLOC_SCRATCH_BYTES
+    assert call(4096, 4 * 10 ** 9) == pace.ERR_SCRATCH_LIMIT
+    assert call(1 << 22, 1000, keep=None) == -1          # argument errors come first
+    assert L.pace_strerror(pace.ERR_SCRATCH_LIMIT) == b"pool too large for the fixed device scratch"
+
+
 def test_select_and_compact_host_argument_errors(L):
     assert L.pace_select(FAKE, 10, 11, FAKE, FAKE, FAKE, 1 << 20, None) == -1     # budget > n
     assert L.pace_select(FAKE, 10, -1, FAKE, FAKE, FAKE, 1 << 20, None) == -1
