@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libpace.so")
-SOURCES = ["score.hip", "select.hip", "compact.hip", "filter_step.hip", "group.hip", "stream.hip", "prefix.hip", "diag.hip", "validate.hip", "noalloc.hip", "pace_abi.cpp"]
+SOURCES = ["score.hip", "select.hip", "select_wide.hip", "compact.hip", "filter_step.hip", "group.hip", "stream.hip", "prefix.hip", "diag.hip", "validate.hip", "noalloc.hip", "pace_abi.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-x", "hip", "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wno-pass-failed",

@@ -197,7 +197,6 @@ __device__ __forceinline__ void copy_range_col(const CompactCols &cols, int col,
 // ---------------------------------------------------------------------------
 constexpr int kPT = 256;                  // threads of a piece workgroup
 constexpr int kPW = kPT / kWave;          // its waves
-constexpr int kPartsPerThread = (int)((kPieceMaxN / kPieceBlock + kPT - 1) / kPT);
 constexpr int kCopyU = 4;                 // 16-byte loads in flight per thread in a piece copy
 
 // Span length of trajectory i if kept (offsets clamped to [0, NT]), else 0.
@@ -213,15 +212,17 @@ __device__ __forceinline__ int64_t kept_span(const int64_t *__restrict__ off, co
     return hi > lo ? hi - lo : 0;
 }
 
-// One wave per block: the block partials from the keep flags.
+// One wave per block of kBlk trajectories: the block partials from the keep
+// flags.
+template <int kBlk>
 __global__ __launch_bounds__(kWave) void compact_partials_kernel(const int64_t *__restrict__ off, int64_t n,
                                                                 int64_t NT, const uint8_t *__restrict__ keep,
                                                                 PieceParts parts) {
     const int lane = lane_id();
-    const int64_t i = (int64_t)blockIdx.x * kPieceBlock + lane;
+    const int64_t i = (int64_t)blockIdx.x * kBlk + lane;
     int64_t len = 0, lo;
     bool kept = false;
-    if (lane < kPieceBlock && i < n) {
+    if (lane < kBlk && i < n) {
         const int64_t k = kept_span(off, keep, i, NT, lo);
         kept = k >= 0;
         len = kept ? k : 0;
@@ -269,11 +270,17 @@ __device__ __forceinline__ void copy_piece(const char *__restrict__ in, char *__
     for (int64_t p = d + t; p < d + m; p += kPT) dst[p] = src[p + delta];
 }
 
+// kBlk trajectories per block (at most a wave); thread t holds the partials
+// of blocks [t*kPP, (t+1)*kPP). offsets_out, kept_ids and n_kept_tokens may
+// be null (rejected ids only).
+template <int kBlk, int kPP>
 __global__ __launch_bounds__(kPT) void compact_piece_kernel(
     const int64_t *__restrict__ off, int64_t n, int64_t NT, const uint8_t *__restrict__ keep,
     PieceParts parts, int64_t nb, CompactCols cols, int n_cols, int64_t *__restrict__ offsets_out,
     int32_t *__restrict__ kept_ids, int64_t *__restrict__ n_kept_tokens, int32_t *__restrict__ reject_ids,
     int64_t budget) {
+    constexpr int kPartsPerThread = kPP;
+    static_assert(kBlk <= kWave, "a block is handled by one wave");
     __shared__ uint32_t w_cnt[kPW], w_pcs[kPW];
     __shared__ int64_t w_len[kPW];
     __shared__ int64_t sel[3];
@@ -306,7 +313,7 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
     uint32_t cb = block_excl_sum_u32<kPW>(cs, tot_c, w_cnt);
     int64_t lb = block_excl_sum_i64<kPW>(ls, tot_l, w_len);
     uint32_t pb = block_excl_sum_u32<kPW>(ps, tot_p, w_pcs);
-    if (q == 0 && t == 0) {
+    if (q == 0 && t == 0 && offsets_out) {
         offsets_out[tot_c] = tot_l;
         *n_kept_tokens = tot_l;
     }
@@ -324,8 +331,8 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
         }
         __syncthreads();
         if (t < kWave) {
-            const int64_t i = q * kPieceBlock + t;
-            const bool in = t < kPieceBlock && i < n;
+            const int64_t i = q * kBlk + t;
+            const bool in = t < kBlk && i < n;
             int64_t len = 0, lo;
             bool kept = false;
             if (in) {
@@ -336,8 +343,10 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
             const int64_t rank = sel[0] + (int64_t)__popcll(ballot(kept) & lanes_below());
             const int64_t dst = sel[1] + (wave_incl_scan_i64(len) - len);
             if (kept) {
-                offsets_out[rank] = dst;
-                kept_ids[rank] = (int32_t)i;
+                if (offsets_out) {
+                    offsets_out[rank] = dst;
+                    kept_ids[rank] = (int32_t)i;
+                }
             } else if (in && reject_ids) {
                 const int64_t rr = i - rank;       // trajectories before i that were rejected
                 if (rr < budget) reject_ids[rr] = (int32_t)i;
@@ -372,9 +381,9 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
         __syncthreads();
         if (t < kWave) {
             const int64_t b = sel[0];
-            const int64_t i = b * kPieceBlock + t;
+            const int64_t i = b * kBlk + t;
             int64_t len = 0, lo = 0;
-            if (t < kPieceBlock && i < n) {
+            if (t < kBlk && i < n) {
                 const int64_t k = kept_span(off, keep, i, NT, lo);
                 len = k > 0 ? k : 0;
             }
@@ -502,10 +511,18 @@ bool compact_piece_ok(int64_t n, int64_t n_tokens) {
     return n <= kPieceMaxN && n_tokens / kPieceLen < ((int64_t)1 << 30);
 }
 
+bool compact_wide_ok(int64_t n, int64_t n_tokens) {
+    return n <= kWideMaxN && n_tokens / kPieceLen < ((int64_t)1 << 30);
+}
+
 hipError_t launch_compact_partials(const int64_t *offsets, int64_t n, int64_t n_tokens,
-                                   const uint8_t *keep, const PieceParts &parts, hipStream_t stream) {
+                                   const uint8_t *keep, const PieceParts &parts, hipStream_t stream,
+                                   int blk) {
     if (n == 0) return hipSuccess;
-    return launch(-1, compact_partials_kernel, dim3((unsigned)piece_blocks(n)), dim3(kWave), stream,
+    if (blk == kWideBlock)
+        return launch(-1, compact_partials_kernel<kWideBlock>, dim3((unsigned)((n + kWideBlock - 1) / kWideBlock)),
+                      dim3(kWave), stream, offsets, n, n_tokens, keep, parts);
+    return launch(-1, compact_partials_kernel<kPieceBlock>, dim3((unsigned)piece_blocks(n)), dim3(kWave), stream,
                   offsets, n, n_tokens, keep, parts);
 }
 
@@ -513,21 +530,34 @@ hipError_t launch_compact_pieces(const int64_t *offsets, int64_t n, int64_t n_to
                                  const PieceParts &parts, const CompactCols &cols, int n_cols,
                                  int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
                                  int32_t *reject_ids, int64_t budget, int64_t max_kept,
-                                 hipStream_t stream) {
+                                 hipStream_t stream, int blk, bool copy) {
     // Block workgroups, then the piece workgroups: a kept span of len tokens
     // has at most len / kPieceLen + 1 pieces, so all kept spans together have
     // at most max_kept + n_tokens / kPieceLen.
     // Past one resident round of workgroups (8 per CU) the piece workgroups
     // loop over the pieces instead.
-    const int64_t nb = piece_blocks(n);
+    const int64_t nb = (n + blk - 1) / blk;
     const int64_t kept_bound = max_kept < 0 ? 0 : (max_kept > n ? n : max_kept);
-    int64_t piece_wgs = kept_bound + n_tokens / kPieceLen + 1;
+    int64_t piece_wgs = copy ? kept_bound + n_tokens / kPieceLen + 1 : 0;
     const int64_t round = resident_waves() / 16 * 8 - nb;
     if (round > 0 && piece_wgs > round) piece_wgs = round;
+    if (copy && piece_wgs < 1) piece_wgs = 1;
     const int64_t grid = (nb > 0 ? nb : 1) + piece_wgs;
-    return launch(kPhaseCompact, compact_piece_kernel, dim3((unsigned)grid), dim3(kPT), stream, offsets, n,
-                  n_tokens, keep, parts, nb, cols, n_cols, offsets_out, kept_ids, n_kept_tokens,
-                  reject_ids, budget);
+    const int64_t per = (nb + kPT - 1) / kPT;
+#define PACE_PIECES(B, P)                                                                                      \
+    return launch(kPhaseCompact, compact_piece_kernel<B, P>, dim3((unsigned)grid), dim3(kPT), stream, offsets, n, \
+                  n_tokens, keep, parts, nb, cols, copy ? n_cols : 0, offsets_out, kept_ids, n_kept_tokens,      \
+                  reject_ids, budget)
+    if (blk == kPieceBlock) {
+        if (per > 2) return hipErrorInvalidValue;
+        PACE_PIECES(kPieceBlock, 2);
+    }
+    if (blk != kWideBlock || per > 16) return hipErrorInvalidValue;
+    if (per <= 2) PACE_PIECES(kWideBlock, 2);
+    if (per <= 4) PACE_PIECES(kWideBlock, 4);
+    if (per <= 8) PACE_PIECES(kWideBlock, 8);
+    PACE_PIECES(kWideBlock, 16);
+#undef PACE_PIECES
 }
 
 hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_tokens,
@@ -546,11 +576,12 @@ hipError_t launch_compact(const int64_t *offsets, int64_t n, int64_t n_tokens, c
                           const CompactCols &cols, int n_cols, int64_t *offsets_out,
                           int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, hipStream_t stream) {
     CompactWs w = compact_ws_carve(ws, n, n_tokens);
-    if (compact_piece_ok(n, n_tokens)) {
-        hipError_t e = launch_compact_partials(offsets, n, n_tokens, keep, w.parts, stream);
+    if (compact_piece_ok(n, n_tokens) || compact_wide_ok(n, n_tokens)) {
+        const int blk = compact_piece_ok(n, n_tokens) ? kPieceBlock : kWideBlock;
+        hipError_t e = launch_compact_partials(offsets, n, n_tokens, keep, w.parts, stream, blk);
         if (e != hipSuccess) return e;
         return launch_compact_pieces(offsets, n, n_tokens, keep, w.parts, cols, n_cols, offsets_out,
-                                     kept_ids, n_kept_tokens, nullptr, 0, n, stream);
+                                     kept_ids, n_kept_tokens, nullptr, 0, n, stream, blk, true);
     }
     compact_scan_kernel<<<1, kT, 0, stream>>>(offsets, n, n_tokens, keep, offsets_out, kept_ids,
                                              n_kept_tokens, w.kept_src, w.chunk_first,

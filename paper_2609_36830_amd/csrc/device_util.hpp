@@ -79,6 +79,12 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) { return (int64_t)wav
 __device__ __forceinline__ uint64_t wave_or_u64(uint64_t v) {
     return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, 0ull, [](uint64_t a, uint64_t b) { return a | b; }), kWave - 1);
 }
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+    return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, ~0ull, [](uint64_t a, uint64_t b) { return a < b ? a : b; }), kWave - 1);
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+    return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, 0ull, [](uint64_t a, uint64_t b) { return a > b ? a : b; }), kWave - 1);
+}
 __device__ __forceinline__ uint64_t wave_and_u64(uint64_t v) {
     return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, ~0ull, [](uint64_t a, uint64_t b) { return a & b; }), kWave - 1);
 }
@@ -164,6 +170,15 @@ __device__ __forceinline__ uint4 load_a4(const void *p) {
 __device__ __forceinline__ void store_nt(uint4 *p, const uint4 &v) {
     const pace_v4u x = {v.x, v.y, v.z, v.w};
     __builtin_nontemporal_store(x, reinterpret_cast<pace_v4u *>(p));
+}
+
+// 64-bit key whose unsigned order is the order of binary64 scores: the
+// sign-magnitude flip, with -0 mapped to +0 (equal scores) and NaN above +inf.
+__device__ __forceinline__ uint64_t score_key(double d) {
+    if (__builtin_isnan(d)) return ~0ull;    // precondition violation: above +inf
+    if (d == 0.0) d = 0.0;                    // -0 and +0 are the same score
+    const uint64_t b = (uint64_t)__double_as_longlong(d);
+    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
 }
 
 __device__ __forceinline__ int64_t clamp64(int64_t v, int64_t lo, int64_t hi) {

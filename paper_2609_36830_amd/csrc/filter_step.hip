@@ -11,8 +11,13 @@
 //                                    per piece of a kept span copies it
 //
 // The same results as pace_score, pace_budget, pace_select and pace_compact
-// called in sequence, in four launches instead of six. Pools beyond the
-// rank and piece limits use those calls' kernels.
+// called in sequence, in four launches instead of six. Pools beyond the rank
+// kernel's limit (8192 trajectories) take the selection spread over the chip
+// instead of the rank (select_wide.hip: the finalize also writes per-group
+// key extremes, then cut_hist, cut_select and classify, which writes the
+// keep flags and the partials of blocks of 64 trajectories) and the same
+// piece compaction; pools beyond that path's limit use the separate calls'
+// kernels.
 #include "device_util.hpp"
 #include "kernels.hpp"
 
@@ -38,13 +43,28 @@ hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64
     p += align256(compact_ws_bytes(n, n_tokens));
     void *sel_ws = p;
 
+    const bool rank_path = n <= kRankMaxN && compact_piece_ok(n, n_tokens);
+    const bool wide_path = !rank_path && compact_wide_ok(n, n_tokens);
+    const WideWs ww = wide_ws_carve(sel_ws, n);
     int64_t chunk_len = 0;
     hipError_t e = launch_score_reduce(tags, offsets, n, n_tokens, V, sws, vec_ok, stream, &chunk_len);
     if (e != hipSuccess) return e;
     e = launch_score_finalize(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix,
-                              w_wait, gamma, chunk_len, score, gen_sum, gen_count, sws, stream);
+                              w_wait, gamma, chunk_len, score, gen_sum, gen_count, sws, stream,
+                              wide_path ? ww.mmin : nullptr, wide_path ? ww.mmax : nullptr);
     if (e != hipSuccess) return e;
-    if (n <= kRankMaxN && compact_piece_ok(n, n_tokens)) {
+    if (wide_path) {
+        const CompactWs cw = compact_ws_carve(cws_base, n, n_tokens);
+        e = launch_wide_cut(score, n, budget, ww, stream);
+        if (e != hipSuccess) return e;
+        e = launch_classify(score, offsets, n, n_tokens, ww, keep, cw.parts, stream);
+        if (e != hipSuccess) return e;
+        const int64_t n_kept = n - (budget < n ? budget : n);
+        return launch_compact_pieces(offsets, n, n_tokens, keep, cw.parts, cols, n_cols, offsets_out,
+                                     kept_ids, n_kept_tokens, reject_ids, budget, n_kept, stream, kWideBlock,
+                                     true);
+    }
+    if (rank_path) {
         const CompactWs cw = compact_ws_carve(cws_base, n, n_tokens);
         e = launch_rank(score, n, budget, keep, offsets, n_tokens, cw.parts, stream);
         if (e != hipSuccess) return e;

@@ -75,11 +75,15 @@ ScoreWorkspace score_ws_carve(void *ws, int64_t n, int64_t n_tokens);
 hipError_t launch_score_reduce(const int32_t *tags, const int64_t *offsets, int64_t n,
                                int64_t n_tokens, int32_t V, const ScoreWorkspace &ws, bool vec_ok,
                                hipStream_t stream, int64_t *chunk_len_out);
+// With mmin/mmax non-null, also writes the smallest and largest score key
+// of each group of kFinGroup trajectories (the wide selection's range).
+constexpr int kFinGroup = 128;
 hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_tokens,
                                  const int32_t *completion, int32_t V, const double *prefix,
                                  const double *window, int64_t W, bool use_prefix, double w_wait,
                                  int gamma, int64_t chunk_len, double *score, int64_t *gen_sum,
-                                 int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream);
+                                 int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream,
+                                 uint64_t *mmin = nullptr, uint64_t *mmax = nullptr);
 hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                         const int32_t *completion, int32_t V, const double *prefix,
                         const double *window, int64_t W, bool use_prefix, double w_wait, int gamma,
@@ -106,12 +110,43 @@ struct PieceParts {
 };
 inline int64_t piece_blocks(int64_t n) { return (n + kPieceBlock - 1) / kPieceBlock; }
 
+// ---- selection spread over the chip (pools beyond kRankMaxN) ----------------
+// The rejection cut: mode 0 rejects nothing, 1 everything, 2 every key >= key,
+// 3 every key > key and the ids <= id among those with key == key.
+struct CutRec {
+    int64_t mode;
+    uint64_t key;
+    int64_t id;
+    int64_t pad;
+};
+constexpr int kWideBlock = 64;          // trajectories per compaction block on the wide path
+constexpr int64_t kWideHistMax = 64;    // histogram workgroups
+constexpr int64_t kWideMaxN = 262144;   // piece compaction limit with wide blocks
+struct WideWs {
+    CutRec *cut;
+    uint64_t *range;
+    uint64_t *mmin, *mmax;   // [n_mm] per group of kFinGroup trajectories
+    uint32_t *hist;          // [kWideHistMax][bins]
+    PieceParts parts;        // [n / kWideBlock] partials when no compaction workspace is at hand
+    int64_t n_mm;
+};
+int64_t wide_hist_wgs(int64_t n);
+size_t wide_select_ws_bytes(int64_t n);
+WideWs wide_ws_carve(void *ws, int64_t n);
+hipError_t launch_key_minmax(const double *score, int64_t n, const WideWs &w, hipStream_t stream);
+hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const WideWs &w, hipStream_t stream);
+
 // keep[i] <- 0 for the `budget` first trajectories in (score desc, id asc).
 // With parts.cnt non-null, also writes the block partials of the keep flags.
 hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,
                        const int64_t *offsets, int64_t n_tokens, const PieceParts &parts,
                        hipStream_t stream);
 size_t select_ws_bytes(int64_t n);
+// offsets may be null (keep flags and kept counts only).
+hipError_t launch_classify(const double *score, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                           const WideWs &w, uint8_t *keep, const PieceParts &parts, hipStream_t stream);
+hipError_t launch_emit_rejects_wide(const uint8_t *keep, int64_t n, const int32_t *kept_cnt, int64_t budget,
+                                    int32_t *reject_ids, hipStream_t stream);
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
                          int32_t *reject_ids, void *ws, hipStream_t stream);
 
@@ -146,13 +181,18 @@ hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_to
 // max_kept bounds the number of kept trajectories (n when unknown); the grid
 // holds max_kept + n_tokens / kPieceLen piece workgroups.
 bool compact_piece_ok(int64_t n, int64_t n_tokens);
+// Blocks of kWideBlock trajectories: pools of up to kWideMaxN.
+bool compact_wide_ok(int64_t n, int64_t n_tokens);
 hipError_t launch_compact_partials(const int64_t *offsets, int64_t n, int64_t n_tokens,
-                                   const uint8_t *keep, const PieceParts &parts, hipStream_t stream);
+                                   const uint8_t *keep, const PieceParts &parts, hipStream_t stream,
+                                   int blk = kPieceBlock);
+// blk: trajectories per block of the partials (kPieceBlock or kWideBlock).
+// copy = false launches the block workgroups only (rejected ids; no columns).
 hipError_t launch_compact_pieces(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                                  const PieceParts &parts, const CompactCols &cols, int n_cols,
                                  int64_t *offsets_out, int32_t *kept_ids, int64_t *n_kept_tokens,
                                  int32_t *reject_ids, int64_t budget, int64_t max_kept,
-                                 hipStream_t stream);
+                                 hipStream_t stream, int blk = kPieceBlock, bool copy = true);
 hipError_t launch_compact(const int64_t *offsets, int64_t n, int64_t n_tokens, const uint8_t *keep,
                           const CompactCols &cols, int n_cols, int64_t *offsets_out,
                           int32_t *kept_ids, int64_t *n_kept_tokens, void *ws, hipStream_t stream);

@@ -283,14 +283,17 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
 
 // Finalize workgroup size: small, so the few thousand trajectories of a pool
 // spread over many CUs.
-constexpr int kFinT = 128;
+constexpr int kFinT = kFinGroup;
 
-template <bool kWinLds>
+// kMinMax: the workgroup also writes the smallest and largest score key of
+// its trajectories (mmin, mmax), the range the wide selection histograms.
+template <bool kWinLds, bool kMinMax>
 __global__ __launch_bounds__(kFinT) void score_finalize_kernel(
     const int64_t *__restrict__ off, int64_t n, int64_t NT, const int32_t *__restrict__ completion,
     int32_t V, const double *__restrict__ prefix, const double *__restrict__ window, int64_t W,
     int use_prefix, double w_wait, int gamma, int64_t chunk_len, ScoreWorkspace ws,
-    double *__restrict__ score, int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count) {
+    double *__restrict__ score, int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count,
+    uint64_t *__restrict__ mmin, uint64_t *__restrict__ mmax) {
     __shared__ double win_lds[kWinLds ? kWindowLdsMax : 1];
     const bool narrow = (NT >> 11) < ((int64_t)1 << 32);   // token positions below 2^43
     // The trajectory's own loads go first (they do not wait for the window),
@@ -315,12 +318,34 @@ __global__ __launch_bounds__(kFinT) void score_finalize_kernel(
         for (int k = (int)threadIdx.x; k < w_n; k += kFinT) win_lds[k] = window[k];
         __syncthreads();
     }
-    if (!in) return;
-    const TrajScore r = score_from_pieces(pc, c, V, use_prefix != 0, s_pre, kWinLds ? win_lds : window, W,
-                                          w_wait, gamma);
-    score[i] = r.score;
-    if (gen_sum) gen_sum[i] = r.S;
-    if (gen_count) gen_count[i] = r.T;
+    if (!kMinMax && !in) return;
+    uint64_t key = 0;
+    if (in) {
+        const TrajScore r = score_from_pieces(pc, c, V, use_prefix != 0, s_pre, kWinLds ? win_lds : window, W,
+                                              w_wait, gamma);
+        score[i] = r.score;
+        if (gen_sum) gen_sum[i] = r.S;
+        if (gen_count) gen_count[i] = r.T;
+        key = score_key(r.score);
+    }
+    if constexpr (kMinMax) {
+        __shared__ uint64_t wl[kFinT / kWave], wh[kFinT / kWave];
+        const uint64_t lo = wave_min_u64(in ? key : ~0ull), hi = wave_max_u64(key);
+        if (lane_id() == 0) {
+            wl[threadIdx.x / kWave] = lo;
+            wh[threadIdx.x / kWave] = hi;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint64_t a = ~0ull, b = 0;
+            for (int w = 0; w < kFinT / kWave; ++w) {
+                a = wl[w] < a ? wl[w] : a;
+                b = wh[w] > b ? wh[w] : b;
+            }
+            mmin[blockIdx.x] = a;
+            mmax[blockIdx.x] = b;
+        }
+    }
 }
 
 }  // namespace
@@ -367,16 +392,22 @@ hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_to
                                  const int32_t *completion, int32_t V, const double *prefix,
                                  const double *window, int64_t W, bool use_prefix, double w_wait,
                                  int gamma, int64_t chunk_len, double *score, int64_t *gen_sum,
-                                 int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream) {
+                                 int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream,
+                                 uint64_t *mmin, uint64_t *mmax) {
     if (n == 0) return hipSuccess;
     const unsigned grid = (unsigned)((n + kFinT - 1) / kFinT);
-    if (use_prefix && W <= kWindowLdsMax)
-        return launch(kPhaseFinalize, score_finalize_kernel<true>, dim3(grid), dim3(kFinT), stream, offsets,
-                      n, n_tokens, completion, V, prefix, window, W, 1, w_wait, gamma, chunk_len, ws,
-                      score, gen_sum, gen_count);
-    return launch(kPhaseFinalize, score_finalize_kernel<false>, dim3(grid), dim3(kFinT), stream, offsets, n,
-                  n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma,
-                  chunk_len, ws, score, gen_sum, gen_count);
+    const bool win_lds = use_prefix && W <= kWindowLdsMax;
+#define PACE_FIN(WIN, MM)                                                                                    \
+    return launch(kPhaseFinalize, score_finalize_kernel<WIN, MM>, dim3(grid), dim3(kFinT), stream, offsets, n, \
+                  n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, chunk_len, ws,   \
+                  score, gen_sum, gen_count, mmin, mmax)
+    if (mmin) {
+        if (win_lds) PACE_FIN(true, true);
+        PACE_FIN(false, true);
+    }
+    if (win_lds) PACE_FIN(true, false);
+    PACE_FIN(false, false);
+#undef PACE_FIN
 }
 
 hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,

@@ -370,7 +370,9 @@ __global__ __launch_bounds__(kT) void emit_rejects_kernel(const uint8_t *__restr
 }  // namespace
 
 size_t select_ws_bytes(int64_t n) {
-    return (n > (int64_t)kT * kSelectMaxItems) ? align256((size_t)n * 8) : 256;
+    const size_t strided = (n > (int64_t)kT * kSelectMaxItems) ? align256((size_t)n * 8) : 256;
+    const size_t wide = wide_select_ws_bytes(n);
+    return strided > wide ? strided : wide;
 }
 
 hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,
@@ -406,6 +408,15 @@ hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t
         else
             emit_rejects_kernel<8><<<1, kT, 0, stream>>>(keep, n, budget, reject_ids);
         return hipGetLastError();
+    }
+    if (n <= kWideMaxN) {
+        // the cut over the chip, keep flags, then the rejected ids in order
+        const WideWs w = wide_ws_carve(ws, n);
+        hipError_t e = launch_key_minmax(score, n, w, stream);
+        if (e == hipSuccess) e = launch_wide_cut(score, n, budget, w, stream);
+        if (e == hipSuccess) e = launch_classify(score, nullptr, n, 0, w, keep, w.parts, stream);
+        if (e == hipSuccess) e = launch_emit_rejects_wide(keep, n, w.parts.cnt, budget, reject_ids, stream);
+        return e;
     }
     if (items <= 16)
         return launch(kPhaseSelect, select_reg_kernel<16>, dim3(1), dim3(kT), stream, score, n, budget,

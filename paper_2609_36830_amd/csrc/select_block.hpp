@@ -38,13 +38,6 @@ struct SelectSmem {
     uint32_t cand_rej[kDirect];
 };
 
-__device__ __forceinline__ uint64_t score_key(double d) {
-    if (__builtin_isnan(d)) return ~0ull;    // precondition violation: above +inf
-    if (d == 0.0) d = 0.0;                    // -0 and +0 are the same score
-    const uint64_t b = (uint64_t)__double_as_longlong(d);
-    return (b >> 63) ? ~b : (b | 0x8000000000000000ull);
-}
-
 __device__ __forceinline__ uint32_t sel_block_excl_scan(uint32_t v, uint32_t &total, uint32_t *wsum) {
     return block_excl_sum_u32<kSelWaves>(v, total, wsum);
 }

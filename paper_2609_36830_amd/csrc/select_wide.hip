@@ -1,0 +1,455 @@
+// Exact top-`budget` selection spread over the chip, for pools beyond the
+// rank kernel's size limit: the Sec. 3.1 rejection rule taken over the current
+// pool as an exact count (score descending, ties to the lower trajectory id),
+// as a cut that any thread can apply to any (key, id).
+//
+// Keys are the 64-bit order-preserving images of the binary64 scores
+// (score_key). Kernels, in order:
+//   key_minmax  (only when the scores do not come from the filter step's
+//               finalize, which writes the same per-group minima and maxima)
+//               per group of trajectories, the smallest and largest key;
+//   cut_hist    up to kWideHistMax workgroups: the global key range [lo, hi] from the
+//               group extremes, then each workgroup histograms its slice of
+//               the keys into kHBins bins of 2^shift keys, (key - lo) >>
+//               shift (monotone in the key), and writes its histogram;
+//   cut_select  one workgroup: sums the histograms and scans the bins from
+//               the top for the bin holding the budget-th largest key. Its
+//               keys (the candidates) are staged in LDS with one pass over
+//               the scores when they fit, and the same bin search repeats on
+//               them with finer bins until at most kPair remain, which are
+//               ranked pairwise by (key desc, id asc). A bin rejected whole
+//               ends the search early; equal keys are ordered by id with an
+//               ordered count. More candidates than LDS holds are refined by
+//               histogramming the scores again from global memory.
+//   classify    one thread per trajectory applies the cut: keep flags, and
+//               per block of kWideBlock trajectories the kept count, kept
+//               tokens and piece count the piece compaction consumes.
+// Every histogram uses LDS atomics on few keys per workgroup, and no kernel
+// needs zeroed memory or an atomic in global memory.
+#include "device_util.hpp"
+#include "kernels.hpp"
+
+namespace pace {
+
+namespace {
+
+constexpr int kHBits = 11;
+constexpr int kHBins = 1 << kHBits;
+constexpr int kWT = 1024;                // threads of the histogram and cut workgroups
+constexpr int kWW = kWT / kWave;
+constexpr int kCandCap = 4096;           // candidates staged in LDS
+constexpr int kPair = 64;                // candidates ranked pairwise (one wave)
+constexpr int kMMT = kFinGroup;          // threads of a min/max workgroup (one key each)
+
+// Bins of 2^shift keys cover [lo, hi] in at most kHBins bins.
+__device__ __forceinline__ int range_shift(uint64_t lo, uint64_t hi) {
+    const uint64_t span = hi - lo;
+    const int L = span ? 64 - __clzll((long long)span) : 0;
+    return L > kHBits ? L - kHBits : 0;
+}
+
+__device__ __forceinline__ bool cut_rejects(const CutRec &c, uint64_t k, int64_t i) {
+    switch (c.mode) {
+        case 0: return false;
+        case 1: return true;
+        case 2: return k >= c.key;
+        default: return k > c.key || (k == c.key && i <= c.id);
+    }
+}
+
+// Smallest and largest key of each group of kMMT scores.
+__global__ __launch_bounds__(kMMT) void key_minmax_kernel(const double *__restrict__ score, int64_t n,
+                                                          uint64_t *__restrict__ mmin, uint64_t *__restrict__ mmax) {
+    __shared__ uint64_t wl[kMMT / kWave], wh[kMMT / kWave];
+    const int64_t i = (int64_t)blockIdx.x * kMMT + threadIdx.x;
+    const uint64_t k = i < n ? score_key(score[i]) : 0ull;
+    const uint64_t lo = wave_min_u64(i < n ? k : ~0ull), hi = wave_max_u64(k);
+    if (lane_id() == 0) {
+        wl[threadIdx.x / kWave] = lo;
+        wh[threadIdx.x / kWave] = hi;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t a = ~0ull, b = 0;
+        for (int w = 0; w < kMMT / kWave; ++w) {
+            a = wl[w] < a ? wl[w] : a;
+            b = wh[w] > b ? wh[w] : b;
+        }
+        mmin[blockIdx.x] = a;
+        mmax[blockIdx.x] = b;
+    }
+}
+
+__global__ __launch_bounds__(kWT) void cut_hist_kernel(const double *__restrict__ score, int64_t n,
+                                                       const uint64_t *__restrict__ mmin,
+                                                       const uint64_t *__restrict__ mmax, int64_t n_mm,
+                                                       int64_t per_wg, uint32_t *__restrict__ hist,
+                                                       uint64_t *__restrict__ range) {
+    __shared__ uint32_t h[kHBins];
+    __shared__ uint64_t wl[kWW], wh[kWW];
+    const int t = threadIdx.x, lane = lane_id(), wv = t / kWave;
+    const int64_t i0 = (int64_t)blockIdx.x * per_wg;
+    const int64_t i1 = (i0 + per_wg < n) ? i0 + per_wg : n;
+    for (int b = t; b < kHBins; b += kWT) h[b] = 0u;
+    uint64_t lo = ~0ull, hi = 0;
+    for (int64_t i = t; i < n_mm; i += kWT) {
+        const uint64_t a = mmin[i], b = mmax[i];
+        lo = a < lo ? a : lo;
+        hi = b > hi ? b : hi;
+    }
+    lo = wave_min_u64(lo);
+    hi = wave_max_u64(hi);
+    if (lane == 0) {
+        wl[wv] = lo;
+        wh[wv] = hi;
+    }
+    __syncthreads();
+    lo = ~0ull;
+    hi = 0;
+#pragma unroll
+    for (int w = 0; w < kWW; ++w) {
+        lo = wl[w] < lo ? wl[w] : lo;
+        hi = wh[w] > hi ? wh[w] : hi;
+    }
+    const int sh = range_shift(lo, hi);
+    for (int64_t i = i0 + t; i < i1; i += 4 * kWT) {
+        uint64_t k[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t j = i + (int64_t)u * kWT;
+            k[u] = j < i1 ? score_key(score[j]) : 0ull;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (i + (int64_t)u * kWT < i1) {
+                const uint64_t d = (k[u] - lo) >> sh;     // below kHBins for keys in [lo, hi]
+                atomicAdd(&h[d < (uint64_t)kHBins ? d : (uint64_t)kHBins - 1], 1u);
+            }
+        }
+    }
+    __syncthreads();
+    for (int b = t; b < kHBins; b += kWT) hist[(int64_t)blockIdx.x * kHBins + b] = h[b];
+    if (blockIdx.x == 0 && t == 0) {
+        range[0] = lo;
+        range[1] = hi;
+    }
+}
+
+__global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restrict__ score, int64_t n,
+                                                         int64_t budget, const uint32_t *__restrict__ hist,
+                                                         int64_t n_hist, const uint64_t *__restrict__ range,
+                                                         CutRec *__restrict__ out) {
+    __shared__ uint32_t h[kHBins];
+    __shared__ uint32_t wsum[kWW];
+    __shared__ uint64_t ck[kCandCap];
+    __shared__ uint32_t ci[kCandCap];
+    __shared__ uint32_t ncand;
+    __shared__ uint64_t s_lo, s_hi, s_key;
+    __shared__ int64_t s_need, s_id;
+    __shared__ uint32_t s_cnt;
+    const int t = threadIdx.x, lane = lane_id();
+    if (budget <= 0 || budget >= n) {
+        if (t == 0) *out = CutRec{budget <= 0 ? 0 : 1, 0, 0, 0};
+        return;
+    }
+    uint64_t lo = range[0], hi = range[1];
+    int64_t need = budget;
+    uint32_t cnt = 0;
+
+    // Descending bin search: thread t holds the counts a, b of digits
+    // kHBins - 1 - 2t and kHBins - 2 - 2t. Narrows [lo, hi] to the bin that
+    // holds the need-th largest candidate.
+    auto pick = [&](uint32_t a, uint32_t b, int sh) {
+        uint32_t tot;
+        const uint32_t ex = block_excl_sum_u32<kWW>(a + b, tot, wsum);
+        if ((int64_t)ex < need && need <= (int64_t)ex + a + b) {
+            const bool first = need <= (int64_t)ex + a;
+            const uint64_t d = first ? (uint64_t)(kHBins - 1 - 2 * t) : (uint64_t)(kHBins - 2 - 2 * t);
+            const uint64_t blo = lo + (d << sh);
+            const uint64_t room = hi - blo, w = (((uint64_t)1 << sh) - 1);
+            s_need = need - (int64_t)(first ? ex : ex + a);
+            s_cnt = first ? a : b;
+            s_lo = blo;
+            s_hi = blo + (room < w ? room : w);
+        }
+        __syncthreads();
+        need = s_need;
+        cnt = s_cnt;
+        lo = s_lo;
+        hi = s_hi;
+        __syncthreads();
+    };
+    auto reject_bin_and_above = [&]() {
+        if (t == 0) *out = CutRec{2, lo, 0, 0};
+    };
+
+    // Level 0: the workgroup histograms.
+    {
+        const int sh = range_shift(lo, hi);
+        uint32_t a = 0, b = 0;
+        for (int64_t g = 0; g < n_hist; ++g) {
+            a += hist[g * kHBins + (kHBins - 1 - 2 * t)];
+            b += hist[g * kHBins + (kHBins - 2 - 2 * t)];
+        }
+        pick(a, b, sh);
+        if (need == (int64_t)cnt) {
+            reject_bin_and_above();
+            return;
+        }
+    }
+
+    // Finer levels until at most kPair candidates remain or they all share
+    // one key (each level splits the key range by 2^kHBits, so six suffice).
+    bool staged = false;
+    for (int level = 0; level < 8 && lo != hi; ++level) {
+        if (!staged && cnt <= (uint32_t)kCandCap) {
+            // One pass over the scores stages every key in [lo, hi].
+            if (t == 0) ncand = 0u;
+            __syncthreads();
+            for (int64_t i = t; i < n; i += 4 * kWT) {
+                uint64_t k[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int64_t j = i + (int64_t)u * kWT;
+                    k[u] = j < n ? score_key(score[j]) : 0ull;
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    const int64_t j = i + (int64_t)u * kWT;
+                    const bool c = j < n && k[u] >= lo && k[u] <= hi;
+                    const uint64_t m = ballot(c);
+                    if (m != 0ull) {
+                        const int leader = __ffsll((long long)m) - 1;
+                        uint32_t base = 0;
+                        if (lane == leader) base = atomicAdd(&ncand, (uint32_t)__popcll(m));
+                        base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
+                        const uint32_t sl = base + (uint32_t)__popcll(m & lanes_below());
+                        if (c && sl < (uint32_t)kCandCap) {
+                            ck[sl] = k[u];
+                            ci[sl] = (uint32_t)j;
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            cnt = ncand < (uint32_t)kCandCap ? ncand : (uint32_t)kCandCap;
+            staged = true;
+        }
+        if (staged && cnt <= (uint32_t)kPair) break;
+        // histogram of the candidates' next digit
+        const int sh = range_shift(lo, hi);
+        for (int b = t; b < kHBins; b += kWT) h[b] = 0u;
+        __syncthreads();
+        if (staged) {
+            for (uint32_t j = (uint32_t)t; j < cnt; j += kWT) {
+                const uint64_t k = ck[j];
+                if (k >= lo && k <= hi) atomicAdd(&h[(k - lo) >> sh], 1u);
+            }
+        } else {
+            for (int64_t i = t; i < n; i += kWT) {
+                const uint64_t k = score_key(score[i]);
+                if (k >= lo && k <= hi) atomicAdd(&h[(k - lo) >> sh], 1u);
+            }
+        }
+        __syncthreads();
+        pick(h[kHBins - 1 - 2 * t], h[kHBins - 2 - 2 * t], sh);
+        if (need == (int64_t)cnt) {
+            reject_bin_and_above();
+            return;
+        }
+        if (staged) {
+            // keep the staged candidates that lie in the new range
+            uint64_t kk[kCandCap / kWT];
+            uint32_t ii[kCandCap / kWT];
+            const uint32_t c_old = ncand < (uint32_t)kCandCap ? ncand : (uint32_t)kCandCap;
+#pragma unroll
+            for (int u = 0; u < kCandCap / kWT; ++u) {
+                const uint32_t j = (uint32_t)t + (uint32_t)u * kWT;
+                kk[u] = j < c_old ? ck[j] : 0ull;
+                ii[u] = j < c_old ? ci[j] : 0u;
+            }
+            __syncthreads();
+            if (t == 0) ncand = 0u;
+            __syncthreads();
+#pragma unroll
+            for (int u = 0; u < kCandCap / kWT; ++u) {
+                const uint32_t j = (uint32_t)t + (uint32_t)u * kWT;
+                const bool c = j < c_old && kk[u] >= lo && kk[u] <= hi;
+                const uint64_t m = ballot(c);
+                if (m != 0ull) {
+                    const int leader = __ffsll((long long)m) - 1;
+                    uint32_t base = 0;
+                    if (lane == leader) base = atomicAdd(&ncand, (uint32_t)__popcll(m));
+                    base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
+                    if (c) {
+                        const uint32_t sl = base + (uint32_t)__popcll(m & lanes_below());
+                        ck[sl] = kk[u];
+                        ci[sl] = ii[u];
+                    }
+                }
+            }
+            __syncthreads();
+            cnt = ncand;
+        }
+    }
+
+    if (lo == hi) {
+        // Every candidate has the key lo: the need-th lowest id among the
+        // trajectories with that key, by an ordered count over ids (thread t
+        // takes ids [t*per, (t+1)*per)).
+        const int64_t per = (n + kWT - 1) / kWT;
+        const int64_t j0 = (int64_t)t * per, j1 = (j0 + per < n) ? j0 + per : n;
+        uint32_t c = 0;
+        for (int64_t j = j0; j < j1; ++j) c += score_key(score[j]) == lo ? 1u : 0u;
+        uint32_t tot;
+        uint32_t before = block_excl_sum_u32<kWW>(c, tot, wsum);
+        if ((int64_t)before < need && need <= (int64_t)before + c) {
+            for (int64_t j = j0; j < j1; ++j) {
+                if (score_key(score[j]) == lo && (int64_t)(++before) == need) {
+                    s_id = j;
+                    break;
+                }
+            }
+        }
+        __syncthreads();
+        if (t == 0) *out = CutRec{3, lo, s_id, 0};
+        return;
+    }
+
+    // At most kPair staged candidates in [lo, hi]: rank them pairwise.
+    if (t < kWave) {
+        const uint32_t c = cnt < (uint32_t)kPair ? cnt : (uint32_t)kPair;
+        if ((uint32_t)t < c) {
+            const uint64_t ka = ck[t];
+            const uint32_t ia = ci[t];
+            uint32_t r = 0;
+            for (uint32_t j = 0; j < c; ++j) {
+                const uint64_t kb = ck[j];
+                const uint32_t ib = ci[j];
+                r += (kb > ka || (kb == ka && ib < ia)) ? 1u : 0u;
+            }
+            if ((int64_t)r == need - 1) {
+                s_key = ka;
+                s_id = ia;
+            }
+        }
+    }
+    __syncthreads();
+    if (t == 0) *out = CutRec{3, s_key, s_id, 0};
+}
+
+// One thread per trajectory: the keep flag from the cut; then the partials
+// of each block of kWideBlock trajectories (one wave): kept count, kept
+// tokens (spans clamped to [0, NT]) and pieces of at most kPieceLen tokens
+// (zero without offsets).
+__global__ __launch_bounds__(256) void classify_kernel(const double *__restrict__ score,
+                                                       const int64_t *__restrict__ off, int64_t n, int64_t NT,
+                                                       const CutRec *__restrict__ cut_p, uint8_t *__restrict__ keep,
+                                                       PieceParts parts) {
+    static_assert(kWideBlock == kWave, "a wide block is one wave");
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const CutRec c = *cut_p;
+    bool kept = false;
+    int64_t len = 0;
+    if (i < n) {
+        const double sc = score[i];
+        int64_t lo = 0, hi = 0;
+        if (off) {
+            lo = clamp64(off[i], 0, NT);
+            hi = clamp64(off[i + 1], 0, NT);
+        }
+        kept = !cut_rejects(c, score_key(sc), i);
+        keep[i] = kept ? 1 : 0;
+        len = kept && hi > lo ? hi - lo : 0;
+    }
+    const uint32_t kc = (uint32_t)__popcll(ballot(kept));
+    const int64_t l = wave_sum_i64(len);
+    const int64_t pc = wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
+    const int64_t b = i / kWideBlock;
+    if (lane_id() == 0 && b * kWideBlock < n) {
+        parts.cnt[b] = (int32_t)kc;
+        parts.len[b] = l;
+        parts.pcs[b] = (int32_t)pc;
+    }
+}
+
+// Rejected ids in ascending order: one wave per block of kWideBlock
+// trajectories; the rejections before the block follow from the kept counts
+// of the blocks before it.
+__global__ __launch_bounds__(kWave) void emit_rejects_wide_kernel(const uint8_t *__restrict__ keep, int64_t n,
+                                                                  const int32_t *__restrict__ kept_cnt,
+                                                                  int64_t budget, int32_t *__restrict__ reject_ids) {
+    const int lane = lane_id();
+    const int64_t b = blockIdx.x;
+    int64_t s = 0;
+    for (int64_t j = lane; j < b; j += kWave) s += kept_cnt[j];
+    s = wave_sum_i64(s);
+    const int64_t i = b * kWideBlock + lane;
+    const bool rej = i < n && keep[i] == 0;
+    const int64_t pos = b * kWideBlock - s + (int64_t)__popcll(ballot(rej) & lanes_below());
+    if (rej && pos < budget) reject_ids[pos] = (int32_t)i;
+}
+
+}  // namespace
+
+int64_t wide_hist_wgs(int64_t n) {
+    const int64_t g = n / 2048;
+    return g < 1 ? 1 : (g > kWideHistMax ? kWideHistMax : g);
+}
+
+size_t wide_select_ws_bytes(int64_t n) {
+    const int64_t mm = (n + kMMT - 1) / kMMT;
+    const int64_t nb = (n + kWideBlock - 1) / kWideBlock;
+    return 256 + align256((size_t)mm * 8) * 2 + align256((size_t)kWideHistMax * kHBins * 4) +
+           align256((size_t)nb * 4) * 2 + align256((size_t)nb * 8);
+}
+
+WideWs wide_ws_carve(void *ws, int64_t n) {
+    const int64_t mm = (n + kMMT - 1) / kMMT;
+    char *p = (char *)ws;
+    WideWs w;
+    w.cut = (CutRec *)p;        p += 64;
+    w.range = (uint64_t *)p;    p += 192;
+    w.mmin = (uint64_t *)p;     p += align256((size_t)mm * 8);
+    w.mmax = (uint64_t *)p;     p += align256((size_t)mm * 8);
+    w.hist = (uint32_t *)p;     p += align256((size_t)kWideHistMax * kHBins * 4);
+    const int64_t nb = (n + kWideBlock - 1) / kWideBlock;
+    w.parts.cnt = (int32_t *)p; p += align256((size_t)nb * 4);
+    w.parts.len = (int64_t *)p; p += align256((size_t)nb * 8);
+    w.parts.pcs = (int32_t *)p;
+    w.n_mm = mm;
+    return w;
+}
+
+hipError_t launch_key_minmax(const double *score, int64_t n, const WideWs &w, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    return launch(kPhaseSelect, key_minmax_kernel, dim3((unsigned)w.n_mm), dim3(kMMT), stream, score, n, w.mmin,
+                  w.mmax);
+}
+
+hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const WideWs &w, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    const int64_t g = wide_hist_wgs(n);
+    const int64_t per = (n + g - 1) / g;
+    hipError_t e = launch(kPhaseSelect, cut_hist_kernel, dim3((unsigned)g), dim3(kWT), stream, score, n, w.mmin,
+                          w.mmax, w.n_mm, per, w.hist, w.range);
+    if (e != hipSuccess) return e;
+    return launch(kPhaseSelect, cut_select_kernel, dim3(1), dim3(kWT), stream, score, n, budget, w.hist, g,
+                  w.range, w.cut);
+}
+
+hipError_t launch_classify(const double *score, const int64_t *offsets, int64_t n, int64_t n_tokens,
+                           const WideWs &w, uint8_t *keep, const PieceParts &parts, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    return launch(kPhaseSelect, classify_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), stream, score,
+                  offsets, n, n_tokens, w.cut, keep, parts);
+}
+
+hipError_t launch_emit_rejects_wide(const uint8_t *keep, int64_t n, const int32_t *kept_cnt, int64_t budget,
+                                    int32_t *reject_ids, hipStream_t stream) {
+    if (n == 0 || budget == 0) return hipSuccess;
+    return launch(kPhaseSelect, emit_rejects_wide_kernel, dim3((unsigned)((n + kWideBlock - 1) / kWideBlock)),
+                  dim3(kWave), stream, keep, n, kept_cnt, budget, reject_ids);
+}
+
+}  // namespace pace

@@ -86,6 +86,12 @@ CONFIGS: Dict[str, dict] = {
     "stress": dict(n=4096, V=5000, capacity=1365, seed=105, kind="lognormal",
                    median=12000.0, sigma=0.185, len_lo=512, len_hi=32768,
                    breaks=("uniform", 0, 16), c_lag=8, last_lag=1),
+    # Scale case beyond the paper's pool sizes: 65536 short trajectories,
+    # LN(median 700) clipped 64..8192 (~52M tokens), 0-4 breaks, V = 5000,
+    # occupancy 3x target (the selection spread over the chip).
+    "wide": dict(n=65536, V=5000, capacity=21845, seed=106, kind="lognormal",
+                 median=700.0, sigma=0.5, len_lo=64, len_hi=8192,
+                 breaks=("uniform", 0, 4), c_lag=8, last_lag=1),
 }
 
 
