@@ -6,22 +6,28 @@
 // 2048 tokens); a chunk is read as 16-byte vectors, 8 per lane in flight, the
 // first batch issued before the trajectory search. (Plain loads on purpose:
 // they leave the tags in the last-level cache, where the compaction re-reads
-// the kept spans.) The wave
-// walks the trajectory boundaries that fall inside its chunk and keeps, per
-// lane, the running piece sum of (tag + 1) over generated tokens (masked
-// tags, -1, add 0) and the generated-token count. When a trajectory ends the
-// wave reduces the piece across lanes and holds it in a lane until the chunk
-// is done, then stores every held piece at once:
-//   - the piece of a trajectory that starts inside this chunk goes to
-//     part_{sum,cnt}[trajectory] (exactly one chunk holds each start);
-//   - the piece of the trajectory that straddles the chunk start goes to
-//     carry_{sum,cnt}[chunk] (at most one per chunk).
+// the kept spans.) Let G(p) be the sum of (tag + 1) over the generated tokens
+// of [chunk start, p) (masked tags, -1, add 0) and their count. The wave holds
+// 64 trajectory offsets, one per lane, and ends with G at each of them
+// (clamped to the chunk); a trajectory's piece in the chunk is then the
+// difference of two neighbouring lanes:
+//   - a block of 1024 tokens without an offset inside is added per lane;
+//   - a block with offsets writes the window-local exclusive prefixes of its
+//     four 256-token windows to LDS (one wave scan per window and quantity),
+//     and each lane whose offset falls in the block reads its G there, so
+//     the cost does not grow with the number of trajectories in the block.
+// The piece of a trajectory that starts inside this chunk goes to
+// part_{sum,cnt}[trajectory] (exactly one chunk holds each start); the piece
+// of the trajectory that straddles the chunk start goes to
+// carry_{sum,cnt}[chunk] (at most one per chunk).
 // No atomics, no zero-filled workspace, and the combine order is fixed, so
 // the integer results are bit-identical run to run.
 //
 // Step 2 (score_finalize): one thread per trajectory adds its carries, forms
 // S_i = c_i T_i - sum(tag) exactly in int64 and evaluates the score of
 // Eq. (6)-(9) in binary64 with a fixed operation order (no contraction).
+#include <type_traits>
+
 #include "device_util.hpp"
 #include "kernels.hpp"
 #include "score_math.hpp"
@@ -39,20 +45,29 @@ constexpr int kSub = 4;                       // windows per fast-path / walk bl
 constexpr int kWavesPerBlock = 4;
 static_assert(kScoreChunkAlign % (kWin * kUnroll) == 0, "chunk must be a multiple of the super-window");
 
-// Lane k caches clamp(off[base + k], 0, NT); reads of increasing indices only.
-struct BoundCache {
-    int64_t base;
-    int64_t val;
-    __device__ __forceinline__ void load(const int64_t *__restrict__ off, int64_t n, int64_t NT, int64_t b) {
-        base = b;
-        int64_t idx = b + lane_id();
-        val = (idx <= n) ? clamp64(off[idx], 0, NT) : NT;
-    }
-    __device__ __forceinline__ int64_t get(const int64_t *__restrict__ off, int64_t n, int64_t NT, int64_t i) {
-        if (i < base || i - base >= kWave) load(off, n, NT, i);
-        return readlane_i64(val, (int)(i - base));
-    }
+// Position-ordered prefixes of one block (kSub windows, kBlk tokens) for the
+// trajectory boundaries inside it, per wave: window-local exclusive prefix
+// sums of (tag + 1) (32-bit when every tag + 1 < 2^24: a window sums below
+// 2^32) and of the generated-token count (at most 255 before the last
+// position of a window, so one byte).
+constexpr int kBlk = kSub * kWin;
+template <bool kNarrow>
+struct BlockPrefix {
+    using S = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
+    S s[kWavesPerBlock][kBlk];
+    uint8_t c[kWavesPerBlock][kBlk];
 };
+
+__device__ __forceinline__ uint32_t wave_incl_add(uint32_t v) { return wave_incl_scan_u32(v); }
+__device__ __forceinline__ uint64_t wave_incl_add(uint64_t v) { return (uint64_t)wave_incl_scan_i64((int64_t)v); }
+
+// The next lane's value (lane 63 gets lane 0's).
+__device__ __forceinline__ int64_t from_next_lane(int64_t v) {
+    const int a = ((lane_id() + 1) & (kWave - 1)) << 2;
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_bpermute(a, (int)(uint32_t)v);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_bpermute(a, (int)(uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 
 // Tags are >= -1, so (tag + 1) summed is the tags' sum plus 4 (mod 2^32; the
 // true partial stays below 2^32), and a tag is masked exactly when its sign
@@ -68,21 +83,6 @@ __device__ __forceinline__ void add_all_wide(const int4 &v, uint64_t &s, uint32_
     uint32_t u2 = (uint32_t)v.z + 1u, u3 = (uint32_t)v.w + 1u;
     s += (uint64_t)u0 + (uint64_t)u1 + (uint64_t)u2 + (uint64_t)u3;
     c += (u0 != 0u) + (u1 != 0u) + (u2 != 0u) + (u3 != 0u);
-}
-
-// Elements of this lane's vector (relative positions r0 .. r0 + 3) that lie
-// in [rlo, rlo + rlen).
-__device__ __forceinline__ void add_range(const int4 &v, uint32_t r0, uint32_t rlo, uint32_t rlen,
-                                          uint64_t &s, uint32_t &c) {
-    const int x[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        if (r0 + (uint32_t)e - rlo < rlen) {
-            const uint32_t u = (uint32_t)x[e] + 1u;
-            s += u;
-            c += (u != 0u);
-        }
-    }
 }
 
 template <bool kVecLoad, int U>
@@ -103,19 +103,24 @@ __device__ __forceinline__ void load_super(const int32_t *__restrict__ tags, int
     }
 }
 
-// kNarrow: every tag + 1 < 2^24, so a lane's 32 tags of one super-window sum
-// below 2^29 in 32 bits before widening.
+// kNarrow: every tag + 1 < 2^24, so a lane's 16 tags of one block sum below
+// 2^28 in 32 bits before widening, and a window's 256 below 2^32.
 template <bool kNarrow, bool kVecLoad, int U = kUnroll>
 __global__ __launch_bounds__(256) void score_reduce_kernel(
     const int32_t *__restrict__ tags, const int64_t *__restrict__ off, int64_t n, int64_t NT,
     int64_t chunk_len, int64_t n_chunks, uint64_t *__restrict__ part_sum,
     int64_t *__restrict__ part_cnt, uint64_t *__restrict__ carry_sum,
     int64_t *__restrict__ carry_cnt) {
+    using PS = typename BlockPrefix<kNarrow>::S;
+    __shared__ BlockPrefix<kNarrow> lds;
     const int lane = lane_id();
-    const int64_t chunk = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x / kWave);
+    const int wv = threadIdx.x / kWave;
+    const int64_t chunk = (int64_t)blockIdx.x * kWavesPerBlock + wv;
     if (chunk >= n_chunks) return;
     const int64_t cs = chunk * chunk_len;
     const int64_t ce = (cs + chunk_len < NT) ? cs + chunk_len : NT;
+    PS *__restrict__ pre_s = lds.s[wv];
+    uint8_t *__restrict__ pre_c = lds.c[wv];
 
     // The first super-window's loads do not depend on the trajectory search:
     // issue them first so the search latency hides under them.
@@ -123,13 +128,14 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
     int4 va[U];
     load_super<kVecLoad>(tags, cs, ce, lane, va);
 
-    // Trajectory that contains the chunk's first token. First guess: the
-    // 64 offsets around the position the token would have if all
-    // trajectories were equally long (one round of loads, which also fills
-    // the bound cache); if the answer is not inside that window, a 64-ary
-    // search over all offsets.
-    BoundCache bc;
-    int64_t s;
+    // Boundary window: lane k holds B = offsets[bb + k] clamped to [0, NT]
+    // (NT past offsets[n]), the start of trajectory bb + k and the end of
+    // trajectory bb + k - 1; the window covers trajectories bb .. bb + 62.
+    // First guess: the 64 offsets around the index the chunk would start at
+    // if all trajectories were equally long; if the trajectory holding the
+    // chunk's first token is not among them, a 64-ary search over all
+    // offsets and one more load.
+    int64_t bb, B;
     {
         const int64_t guess = NT > 0 ? (int64_t)((double)cs / (double)NT * (double)n) : 0;
         const int64_t top = (n + 1 > kWave) ? n + 1 - kWave : 0;
@@ -140,112 +146,161 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
         const bool lo_ok = base == 0 || (m & 1ull);
         const bool hi_ok = base + kWave > n || !(m >> (kWave - 1));
         if (lo_ok && hi_ok) {
-            s = base + (int64_t)__popcll(m) - 1;
-            bc.base = base;
-            bc.val = (idx <= n) ? clamp64(raw, 0, NT) : NT;
+            bb = base;
+            B = (idx <= n) ? clamp64(raw, 0, NT) : NT;
         } else {
-            s = wave_last_le(off, n, cs);
-            bc.base = INT64_MIN / 2;          // empty: the first get() loads
-            bc.val = 0;
+            const int64_t s = wave_last_le(off, n, cs);
+            bb = s < 0 ? 0 : s;
+            const int64_t i2 = bb + lane;
+            B = (i2 <= n) ? clamp64(off[i2], 0, NT) : NT;
         }
     }
-    int64_t cur, cur_end;
-    bool valid = false, pending = false, carry_piece = false;
-    if (s < 0) {                 // only for malformed offsets: tokens before offsets[0]
-        cur = -1;
-        cur_end = bc.get(off, n, NT, 0);
-    } else if (s >= n) {         // tokens at or past offsets[n]
-        cur = n;
-        cur_end = INT64_MAX;
-    } else {
-        cur = s;
-        const int64_t cur_start = bc.get(off, n, NT, s);
-        cur_end = bc.get(off, n, NT, s + 1);
-        valid = true;
-        pending = true;
-        carry_piece = cur_start < cs;
-    }
+    // The next boundary window, loaded ahead when the chunk may reach it.
+    int64_t nB = NT;
+    bool nB_ok = false;
+    auto load_next = [&]() {
+        const int64_t i2 = bb + (kWave - 1) + lane;
+        nB = (i2 <= n) ? clamp64(off[i2], 0, NT) : NT;
+        nB_ok = true;
+    };
+    auto want_next = [&]() { return !nB_ok && bb + (kWave - 1) < n && readlane_i64(B, kWave - 1) < ce; };
+    if (want_next()) load_next();
 
-    uint64_t acc_s = 0;
+    // G(p): sum of (tag + 1) over generated tokens and their count in
+    // [cs, p). Lane k ends with G(clamp(B, cs, ce)), so a trajectory's piece
+    // in this chunk is the difference of two neighbouring lanes.
+    uint64_t Gs = 0;
+    int64_t Gc = 0;
+    uint64_t Ws = 0;             // G at the current block's start, less what acc_* still hold
+    int64_t Wc = 0;
+    uint64_t acc_s = 0;          // per-lane sums of blocks without a boundary
     uint32_t acc_c = 0;
+    bool dirty = false;
+    auto sync = [&]() {
+        if (dirty) {
+            Ws += wave_sum_u64(acc_s);
+            Wc += (int64_t)wave_sum_u64((uint64_t)acc_c);
+            acc_s = 0;
+            acc_c = 0;
+            dirty = false;
+        }
+    };
+    // Smallest boundary still ahead (wave-uniform).
+    int64_t next_b;
+    {
+        const uint64_t m = ballot(B > cs);
+        next_b = m ? readlane_i64(B, __ffsll((long long)m) - 1) : INT64_MAX;
+    }
 
-    // Finished pieces wait in registers, the k-th in lane k, and are stored
-    // after the last super-window: a store in mid-stream would hold up the
-    // next loads (the vector memory counter covers stores too). Past 64
-    // pieces a chunk stores directly.
-    int n_held = 0;                     // wave-uniform
+    // Pieces of the window's trajectories (lane k: trajectory bb + k):
+    // at = trajectory for a piece that starts in this chunk, -1 for the piece
+    // that straddles the chunk start, -2 for none. The first window finished
+    // mid-chunk waits in held_* and is stored after the last super-window (a
+    // store in mid-stream would hold up the next loads: one counter covers
+    // loads and stores).
+    int64_t held_at = -2, held_c = 0;
     uint64_t held_s = 0;
-    int64_t held_c = 0, held_at = 0;    // held_at: trajectory, or -1 for the carry
-    auto store_piece = [&](int64_t at, uint64_t ts, int64_t tc) {
-        if (at < 0) {
-            carry_sum[chunk] = ts;
-            carry_cnt[chunk] = tc;
-        } else {
-            part_sum[at] = ts;
-            part_cnt[at] = tc;
+    auto store_piece = [&](int64_t at, uint64_t ps, int64_t pc) {
+        if (at >= 0) {
+            part_sum[at] = ps;
+            part_cnt[at] = pc;
+        } else if (at == -1) {
+            carry_sum[chunk] = ps;
+            carry_cnt[chunk] = pc;
         }
     };
-    auto flush = [&]() {
-        const uint64_t ts = wave_sum_u64(acc_s);
-        const int64_t tc = (int64_t)wave_sum_u64((uint64_t)acc_c);
-        const int64_t at = carry_piece ? -1 : cur;
-        if (n_held < kWave) {
-            if (lane == n_held) {
-                held_s = ts;
-                held_c = tc;
-                held_at = at;
-            }
-            ++n_held;
-        } else if (lane == 0) {
-            store_piece(at, ts, tc);
-        }
-        acc_s = 0;
-        acc_c = 0;
+    auto pieces = [&](int64_t &at, uint64_t &ps, int64_t &pc) {
+        const int64_t B1 = from_next_lane(B);
+        ps = (uint64_t)from_next_lane((int64_t)Gs) - Gs;
+        pc = from_next_lane(Gc) - Gc;
+        const int64_t j = bb + lane;
+        const bool has = lane < kWave - 1 && j < n && B1 > B && B < ce && B1 > cs;
+        at = !has ? -2 : (B >= cs ? j : -1);
+    };
+    // Every boundary of the window lies before the current block's end:
+    // keep its pieces and move to the next window.
+    auto next_window = [&]() {
+        int64_t at, pc;
+        uint64_t ps;
+        pieces(at, ps, pc);
+        if (held_at != -2) store_piece(held_at, held_s, held_c);
+        held_at = at;
+        held_s = ps;
+        held_c = pc;
+        const uint64_t g_s = (uint64_t)readlane_i64((int64_t)Gs, kWave - 1);
+        const int64_t g_c = readlane_i64(Gc, kWave - 1);
+        if (!nB_ok) load_next();
+        bb += kWave - 1;
+        B = nB;
+        nB_ok = false;
+        Gs = lane == 0 ? g_s : 0ull;
+        Gc = lane == 0 ? g_c : 0;
     };
 
-    // Boundary walk over the kSub vectors at vb (tokens [bpos, bend)): walk
-    // the trajectory ends in order; for each trajectory piece every lane adds
-    // its tags whose positions fall in the piece.
-    auto walk = [&](int4 *vb, int64_t bpos, int64_t bend) {
-        int64_t lo = bpos;
-        while (true) {
-            const int64_t hi = cur_end < bend ? cur_end : bend;
-            if (valid && hi > lo) {
-                // Keep the per-tag work inside this loop: hoisted out of it,
-                // it would hold every tag's (tag + 1) live at once.
+    // A block holding boundaries: window-local prefixes into LDS, then every
+    // lane whose boundary falls in the block reads its G.
+    auto slow_block = [&](const int4 *v, int64_t bpos, int64_t bend) {
+        sync();
+        uint64_t wpre_s[kSub];
+        int64_t wpre_c[kSub];
+        uint64_t run_s = 0;
+        int64_t run_c = 0;
 #pragma unroll
-                for (int k = 0; k < kSub; ++k)
-                    asm volatile("" : "+v"(vb[k].x), "+v"(vb[k].y), "+v"(vb[k].z), "+v"(vb[k].w));
-                // Positions relative to the block fit in 32 bits.
-                const uint32_t rlo = (uint32_t)(lo - bpos), rlen = (uint32_t)(hi - lo);
-                uint64_t ps = 0;
-                uint32_t pc = 0;
-#pragma unroll
-                for (int k = 0; k < kSub; ++k)
-                    add_range(vb[k], (uint32_t)(k * kWin + lane * kVec), rlo, rlen, ps, pc);
-                acc_s += ps;
-                acc_c += pc;
-            }
-            if (cur_end > bend) break;            // trajectory continues past this block
-            if (pending) flush();                 // trajectory `cur` ends at cur_end
-            lo = cur_end;
-            ++cur;
-            while (cur < n && bc.get(off, n, NT, cur + 1) <= lo) ++cur;   // skip empty ones
-            carry_piece = false;
-            if (cur >= n) {
-                valid = false;
-                pending = false;
-                cur_end = INT64_MAX;
+        for (int k = 0; k < kSub; ++k) {
+            wpre_s[k] = run_s;
+            wpre_c[k] = run_c;
+            const uint32_t u0 = (uint32_t)v[k].x + 1u, u1 = (uint32_t)v[k].y + 1u;
+            const uint32_t u2 = (uint32_t)v[k].z + 1u, u3 = (uint32_t)v[k].w + 1u;
+            const PS p1 = (PS)u0, p2 = p1 + (PS)u1, p3 = p2 + (PS)u2, p4 = p3 + (PS)u3;
+            const uint32_t c1 = (u0 != 0u), c2 = c1 + (u1 != 0u), c3 = c2 + (u2 != 0u), c4 = c3 + (u3 != 0u);
+            const PS is = wave_incl_add(p4);
+            const uint32_t ic = wave_incl_scan_u32(c4);
+            const PS es = is - p4;
+            const uint32_t ec = ic - c4;
+            PS *ds = pre_s + k * kWin + lane * kVec;
+            ds[0] = es;
+            ds[1] = es + p1;
+            ds[2] = es + p2;
+            ds[3] = es + p3;
+            *reinterpret_cast<uint32_t *>(pre_c + k * kWin + lane * kVec) =
+                ec | ((ec + c1) << 8) | ((ec + c2) << 16) | ((ec + c3) << 24);
+            if constexpr (kNarrow) {
+                run_s += (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)is, kWave - 1);
             } else {
-                valid = true;
-                cur_end = bc.get(off, n, NT, cur + 1);
-                pending = lo < ce;
+                run_s += (uint64_t)readlane_i64((int64_t)is, kWave - 1);
             }
-            if (lo >= bend) break;
+            run_c += (int64_t)(uint32_t)__builtin_amdgcn_readlane((int)ic, kWave - 1);
         }
+        while (true) {
+            if (B >= bpos && B < bend) {
+                const int q = (int)(B - bpos);
+                const int k = q / kWin;
+                uint64_t ws = wpre_s[0];
+                int64_t wc = wpre_c[0];
+#pragma unroll
+                for (int kk = 1; kk < kSub; ++kk) {
+                    ws = k == kk ? wpre_s[kk] : ws;
+                    wc = k == kk ? wpre_c[kk] : wc;
+                }
+                Gs = Ws + ws + (uint64_t)pre_s[q];
+                Gc = Wc + wc + (int64_t)pre_c[q];
+            }
+            const uint64_t m = ballot(B >= bend);
+            if (m) {
+                next_b = readlane_i64(B, __ffsll((long long)m) - 1);
+                break;
+            }
+            if (bb + (kWave - 1) >= n) {          // no trajectory after this window
+                next_b = INT64_MAX;
+                break;
+            }
+            next_window();
+        }
+        Ws += run_s;
+        Wc += run_c;
     };
 
-    // Adds the kSub vectors at vb (all inside trajectory `cur`).
+    // Adds the kSub vectors at vb (a block without boundaries).
     auto add_block = [&](const int4 *vb) {
         if (kNarrow) {
             uint32_t s32 = 0, c32 = 0;
@@ -257,28 +312,33 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
 #pragma unroll
             for (int k = 0; k < kSub; ++k) add_all_wide(vb[k], acc_s, acc_c);
         }
-    };
-
-    // Adds the super-window at `pos` (held in v) to the running pieces: whole
-    // blocks of kSub vectors inside trajectory `cur` take the fast path, a
-    // block holding a trajectory end is walked.
-    auto process = [&](int4 (&v)[U], int64_t pos) {
-#pragma unroll
-        for (int h = 0; h < U / kSub; ++h) {
-            const int64_t bpos = pos + (int64_t)h * kSub * kWin;
-            if (bpos >= ce) break;
-            const int64_t bend = (bpos + kSub * kWin < ce) ? bpos + kSub * kWin : ce;
-            if (valid && cur_end >= bend) add_block(v + h * kSub);
-            else walk(v + h * kSub, bpos, bend);
-        }
+        dirty = true;
     };
 
     for (int64_t pos = cs; pos < ce; pos += kSuper) {
-        if (pos != cs) load_super<kVecLoad>(tags, pos, ce, lane, va);
-        process(va, pos);
+        if (pos != cs) {
+            if (want_next()) load_next();
+            load_super<kVecLoad>(tags, pos, ce, lane, va);
+        }
+#pragma unroll
+        for (int h = 0; h < U / kSub; ++h) {
+            const int64_t bpos = pos + (int64_t)h * kBlk;
+            if (bpos >= ce) break;
+            const int64_t bend = (bpos + kBlk < ce) ? bpos + kBlk : ce;
+            if (next_b >= bend) add_block(va + h * kSub);
+            else slow_block(va + h * kSub, bpos, bend);
+        }
     }
-    if (pending) flush();
-    if (lane < n_held) store_piece(held_at, held_s, held_c);
+    sync();
+    if (B >= ce) {
+        Gs = Ws;
+        Gc = Wc;
+    }
+    int64_t at, pc;
+    uint64_t ps;
+    pieces(at, ps, pc);
+    store_piece(at, ps, pc);
+    store_piece(held_at, held_s, held_c);
 }
 
 // Finalize workgroup size: small, so the few thousand trajectories of a pool

@@ -245,6 +245,16 @@ def test_large_versions_take_the_wide_path(pace, fused):
 
 
 @FUSED
+def test_large_versions_many_boundaries(pace, fused):
+    """64-bit window prefixes: short trajectories put boundaries in most
+    blocks of the reduction while tag + 1 reaches 2^30."""
+    lens = np.random.default_rng(31).integers(0, 300, size=3000)
+    pool = poolgen.make_custom_pool(lens, V=2 ** 30, seed=31, mask_frac=0.2, W=64)
+    say("wide versions, short trajectories fused %s" % fused)
+    assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), "wide short")
+
+
+@FUSED
 @pytest.mark.parametrize("gamma", [1, 2, 3, 4])
 def test_gamma_and_window_min(pace, gamma, fused):
     pool = poolgen.make_pool("math", n=400)
