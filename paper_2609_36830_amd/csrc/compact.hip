@@ -27,6 +27,15 @@
 // many workgroups, long enough that the per-workgroup set-up is small next to
 // the copy.
 //
+// Wide blocks (kWideBlock = 64 trajectories, pools up to kWideMaxN): the kept
+// spans of a block are mostly short, so one span per piece would leave every
+// piece workgroup mostly set-up. Spans longer than kPieceLen still make
+// pieces; the shorter ones of a block are copied together as segments of
+// kSegLen tokens: the block's own workgroup copies the first right after its
+// index outputs, piece workgroups the rest. A segment copy lays a table of
+// 16-byte destination slots over its spans in LDS, so each thread keeps
+// several loads in flight whatever the span lengths.
+//
 // Scan path (larger pools): one workgroup scans the flags into the packed
 // offsets, kept ids, span sources and a map from each output chunk of
 // kCopyChunk elements to its first span; a second kernel copies.
@@ -213,7 +222,7 @@ __device__ __forceinline__ int64_t kept_span(const int64_t *__restrict__ off, co
 }
 
 // One wave per block of kBlk trajectories: the block partials from the keep
-// flags.
+// flags (pieces as wide_block_pieces counts them for wide blocks).
 template <int kBlk>
 __global__ __launch_bounds__(kWave) void compact_partials_kernel(const int64_t *__restrict__ off, int64_t n,
                                                                 int64_t NT, const uint8_t *__restrict__ keep,
@@ -229,7 +238,10 @@ __global__ __launch_bounds__(kWave) void compact_partials_kernel(const int64_t *
     }
     const uint32_t c = (uint32_t)__popcll(ballot(kept));
     const int64_t l = wave_sum_i64(len);
-    const int64_t pc = wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
+    const int64_t pc = kBlk == kWideBlock
+        ? wide_block_pieces(wave_sum_i64(len > kPieceLen ? (len + kPieceLen - 1) / kPieceLen : 0),
+                            wave_sum_i64(len > kPieceLen ? 0 : len))
+        : wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
     if (lane == 0) {
         parts.cnt[blockIdx.x] = (int32_t)c;
         parts.len[blockIdx.x] = l;
@@ -270,6 +282,117 @@ __device__ __forceinline__ void copy_piece(const char *__restrict__ in, char *__
     for (int64_t p = d + t; p < d + m; p += kPT) dst[p] = src[p + delta];
 }
 
+// The workgroup copies one segment of a wide block: lane j of wave 0 brings
+// destination range [a, b) of span j (empty when span j has no part in the
+// segment) and del = source - destination, in elements. The slots are, for
+// columns of 4- or 8-byte elements with 16-byte aligned pointers, the aligned
+// 16-byte destination vectors inside each range (in bytes; sources are at
+// least 4-byte aligned), else single elements; a segment has at most kSegLen
+// elements. The slots' prefix over the spans goes to LDS; each thread takes
+// slots t, t + kPT, ... (kSegU loads in flight, each slot's span by a
+// six-step binary search), and with vectors the lanes of wave 0 copy the few
+// bytes at their range's ends.
+constexpr int kSegU = 8;
+struct SegTable {
+    int32_t start[kWave + 1];   // first slot of each span; [kWave] = slots in the segment
+    int64_t dst[kWave];         // destination of each span's first slot (bytes or elements)
+    int64_t src[kWave];         // its source
+};
+
+// Span j holding slot g.
+__device__ __forceinline__ int seg_find(const SegTable &tb, int32_t g) {
+    int j = 0;
+#pragma unroll
+    for (int step = kWave / 2; step > 0; step >>= 1) j = tb.start[j + step] <= g ? j + step : j;
+    return j;
+}
+
+// Builds the slot table (wave 0) from per-lane ranges [a, b) in units of
+// `unit` and source shift del; slots are groups of `per` units at multiples
+// of `per`, units outside them go through `edge` (called by the lane).
+template <typename Edge>
+__device__ __forceinline__ void seg_table(SegTable &tb, int64_t a, int64_t b, int64_t del, int per, Edge edge) {
+    int64_t v0 = (a + per - 1) / per, v1 = b / per;
+    if (v1 < v0) v1 = v0;
+    const int32_t cnt = (int32_t)(v1 - v0);
+    const int32_t incl = (int32_t)wave_incl_scan_u32((uint32_t)cnt);
+    const int t = threadIdx.x;
+    tb.start[t] = incl - cnt;
+    if (t == kWave - 1) tb.start[kWave] = incl;
+    tb.dst[t] = v0 * per;
+    tb.src[t] = v0 * per + del;
+    const int64_t h = cnt > 0 ? v0 * per : b;
+    for (int64_t p = a; p < h; ++p) edge(p);
+    if (cnt > 0)
+        for (int64_t p = v1 * per; p < b; ++p) edge(p);
+}
+
+// 16-byte vector slots over byte ranges.
+__device__ void copy_segment_vec(const char *__restrict__ in, char *__restrict__ out, int64_t a, int64_t b,
+                                 int64_t del, SegTable &tb) {
+    const int t = threadIdx.x;
+    __syncthreads();                           // the previous column's table is no longer read
+    if (t < kWave) seg_table(tb, a, b, del, 16, [&](int64_t p) { out[p] = in[p + del]; });
+    __syncthreads();
+    const int32_t total = tb.start[kWave];
+    for (int32_t g0 = t; g0 < total; g0 += kSegU * kPT) {
+        uint32_t jr[kSegU];                    // span << 26 | slot in span; ~0: none
+        uint4 x[kSegU];
+#pragma unroll
+        for (int u = 0; u < kSegU; ++u) {
+            const int32_t g = g0 + u * kPT;
+            jr[u] = ~0u;
+            if (g < total) {
+                const int j = seg_find(tb, g);
+                const int32_t r = g - tb.start[j];
+                jr[u] = ((uint32_t)j << 26) | (uint32_t)r;
+                x[u] = load_a4(in + tb.src[j] + (int64_t)r * 16);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kSegU; ++u)
+            if (jr[u] != ~0u)
+                store_nt(reinterpret_cast<uint4 *>(out + tb.dst[jr[u] >> 26] + (int64_t)(jr[u] & 0x3ffffffu) * 16),
+                         x[u]);
+    }
+}
+
+// Single-element slots.
+template <int E>
+__device__ void copy_segment_elem(const char *__restrict__ in, char *__restrict__ out, int64_t a, int64_t b,
+                                  int64_t del, SegTable &tb) {
+    using T = typename Elem<E>::T;
+    const T *src = reinterpret_cast<const T *>(in);
+    T *dst = reinterpret_cast<T *>(out);
+    const int t = threadIdx.x;
+    __syncthreads();
+    if (t < kWave) seg_table(tb, a, b, del, 1, [&](int64_t) {});
+    __syncthreads();
+    const int32_t total = tb.start[kWave];
+    for (int32_t g = t; g < total; g += kPT) {
+        const int j = seg_find(tb, g);
+        const int64_t r = g - tb.start[j];
+        dst[tb.dst[j] + r] = src[tb.src[j] + r];
+    }
+}
+
+__device__ __forceinline__ void copy_segment_col(const CompactCols &cols, int col, int64_t a, int64_t b, int64_t del,
+                                                 SegTable &tb) {
+    const char *in = (const char *)cols.in[col];
+    char *out = (char *)cols.out[col];
+    const int E = cols.elem[col];
+    if (cols.vec[col] != 0 && E >= 4) {
+        copy_segment_vec(in, out, a * E, b * E, del * E, tb);
+        return;
+    }
+    switch (E) {
+        case 1: copy_segment_elem<1>(in, out, a, b, del, tb); break;
+        case 2: copy_segment_elem<2>(in, out, a, b, del, tb); break;
+        case 4: copy_segment_elem<4>(in, out, a, b, del, tb); break;
+        default: copy_segment_elem<8>(in, out, a, b, del, tb); break;
+    }
+}
+
 // kBlk trajectories per block (at most a wave); thread t holds the partials
 // of blocks [t*kPP, (t+1)*kPP). offsets_out, kept_ids and n_kept_tokens may
 // be null (rejected ids only).
@@ -290,6 +413,21 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
     if (t == 0) {
         sel[0] = sel[1] = sel[2] = 0;
         piece[0] = piece[1] = piece[2] = 0;   // an unmatched piece copies nothing
+    }
+    // Wide block workgroups: the block's spans, loaded with the partials
+    // (flag and offsets together: one round trip). len -1: rejected.
+    int64_t b_lo = 0, b_len = -1;
+    if constexpr (kBlk == kWideBlock) {
+        const int64_t i = q * kBlk + t;
+        if (q < nb && t < kWave && i < n) {
+            const uint8_t kf = keep[i];
+            const int64_t a = off[i], b = off[i + 1];
+            if (kf != 0) {
+                b_lo = clamp64(a, 0, NT);
+                const int64_t hi = clamp64(b, 0, NT);
+                b_len = hi > b_lo ? hi - b_lo : 0;
+            }
+        }
     }
 
     // 1. Exclusive prefix of the block partials; thread t holds blocks
@@ -330,12 +468,17 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
             lb += l[k];
         }
         __syncthreads();
+        int64_t a = 0, e = 0, del = 0;         // wide: span t's part of the block's first segment
         if (t < kWave) {
             const int64_t i = q * kBlk + t;
             const bool in = t < kBlk && i < n;
-            int64_t len = 0, lo;
+            int64_t len = 0, lo = 0;
             bool kept = false;
-            if (in) {
+            if constexpr (kBlk == kWideBlock) {
+                kept = b_len >= 0;
+                len = kept ? b_len : 0;
+                lo = b_lo;
+            } else if (in) {
                 const int64_t k = kept_span(off, keep, i, NT, lo);
                 kept = k >= 0;
                 len = kept ? k : 0;
@@ -351,13 +494,130 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
                 const int64_t rr = i - rank;       // trajectories before i that were rejected
                 if (rr < budget) reject_ids[rr] = (int32_t)i;
             }
+            if constexpr (kBlk == kWideBlock) {
+                const int64_t sl = len > kPieceLen ? 0 : len;
+                const int64_t f = wave_incl_scan_i64(sl) - sl;
+                const int64_t fb = (f + sl < kSegLen) ? f + sl : kSegLen;
+                if (fb > f) {
+                    a = dst;
+                    e = dst + (fb - f);
+                    del = lo - dst;
+                    if (e > NT) e = NT;                // overlapping (malformed) offsets overflow the output
+                    if (a > e) a = e;
+                }
+            }
+        }
+        if constexpr (kBlk == kWideBlock) {
+            __shared__ SegTable tb0;
+            for (int col = 0; col < n_cols; ++col) copy_segment_col(cols, col, a, e, del, tb0);
         }
         return;
     }
 
     // 2b. Pieces q - nb, q - nb + stride, ... (stride = piece workgroups in
-    //     the grid): for each, its block, then its trajectory in the block.
+    //     the grid): for each, its block, then its trajectory in the block
+    //     (wide blocks: a piece of a long span, or a segment of the short ones
+//     after the first, which the block's workgroup copies).
     const int64_t stride = (int64_t)gridDim.x - nb;
+    if constexpr (kBlk == kWideBlock) {
+        __shared__ SegTable tb;
+        __shared__ int sg_mode;
+        // The blocks' piece and token prefixes move to LDS, so that no
+        // register holds them while the pieces are copied.
+        __shared__ uint32_t s_pb[kPT * kPartsPerThread + 1];
+        __shared__ int64_t s_lb[kPT * kPartsPerThread];
+        {
+            uint32_t pbk = pb;
+            int64_t lbk = lb;
+#pragma unroll
+            for (int k = 0; k < kPartsPerThread; ++k) {
+                s_pb[t * kPartsPerThread + k] = pbk;
+                s_lb[t * kPartsPerThread + k] = lbk;
+                pbk += pc[k];
+                lbk += l[k];
+            }
+            if (t == kPT - 1) s_pb[kPT * kPartsPerThread] = pbk;
+        }
+        for (int64_t pq = q - nb; pq < (int64_t)tot_p; pq += stride) {
+            __syncthreads();                   // the previous piece's reads of sel/piece/sg_mode are done
+            if (t == 0) {
+                sel[0] = sel[1] = sel[2] = 0;
+                piece[0] = piece[1] = piece[2] = 0;
+                sg_mode = 0;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < kPartsPerThread; ++k) {
+                const int b = t * kPartsPerThread + k;
+                const uint32_t p0 = s_pb[b], p1 = s_pb[b + 1];
+                if (b < nb && (int64_t)p0 <= pq && pq < (int64_t)p1) {
+                    sel[0] = b;
+                    sel[1] = p0;
+                    sel[2] = s_lb[b];
+                }
+            }
+            __syncthreads();
+            int64_t a = 0, e = 0, del = 0;     // wave 0, lane j: span j's destination range and shift
+            if (t < kWave) {
+                const int64_t i = sel[0] * kBlk + t;
+                int64_t len = 0, lo = 0;
+                if (i < n) {
+                    const int64_t k = kept_span(off, keep, i, NT, lo);
+                    len = k > 0 ? k : 0;
+                }
+                const int64_t dst = sel[2] + (wave_incl_scan_i64(len) - len);
+                const bool lng = len > kPieceLen;
+                const int64_t np = lng ? (len + kPieceLen - 1) / kPieceLen : 0;
+                const int64_t np_incl = wave_incl_scan_i64(np);
+                const int64_t n_long = readlane_i64(np_incl, kWave - 1);
+                const int64_t qq = pq - sel[1];
+                if (qq < n_long) {
+                    if (np > 0 && np_incl - np <= qq && qq < np_incl) {
+                        const int64_t k = qq - (np_incl - np);
+                        piece[0] = dst + k * kPieceLen;
+                        piece[1] = lo + k * kPieceLen;
+                        piece[2] = (len - k * kPieceLen) < kPieceLen ? len - k * kPieceLen : kPieceLen;
+                    }
+                    if (t == 0) sg_mode = 1;
+                } else {
+                    const int64_t sl = lng ? 0 : len;
+                    const int64_t f = wave_incl_scan_i64(sl) - sl;     // span's start among the short tokens
+                    const int64_t s0 = (qq - n_long + 1) * kSegLen, s1 = s0 + kSegLen;
+                    const int64_t fa = f > s0 ? f : s0, fb = (f + sl < s1) ? f + sl : s1;
+                    if (fb > fa) {
+                        a = dst + (fa - f);
+                        e = dst + (fb - f);
+                        del = lo - dst;
+                        if (e > NT) e = NT;            // overlapping (malformed) offsets overflow the output
+                        if (a > e) a = e;
+                    }
+                    if (t == 0) sg_mode = 2;
+                }
+            }
+            __syncthreads();
+            const int mode = sg_mode;
+            if (mode == 2) {
+                for (int col = 0; col < n_cols; ++col) copy_segment_col(cols, col, a, e, del, tb);
+                continue;
+            }
+            const int64_t d = piece[0], s = piece[1];
+            int64_t m = piece[2];
+            if (mode != 1 || d >= NT || m <= 0) continue;
+            if (d + m > NT) m = NT - d;
+            for (int col = 0; col < n_cols; ++col) {
+                const char *in = (const char *)cols.in[col];
+                char *out = (char *)cols.out[col];
+                const bool vec = cols.vec[col] != 0;
+                switch (cols.elem[col]) {
+                    case 1: copy_piece<1>(in, out, vec, d, s, m); break;
+                    case 2: copy_piece<2>(in, out, vec, d, s, m); break;
+                    case 4: copy_piece<4>(in, out, vec, d, s, m); break;
+                    default: copy_piece<8>(in, out, vec, d, s, m); break;
+                }
+            }
+        }
+        return;
+    }
     for (int64_t pq = q - nb; pq < (int64_t)tot_p; pq += stride) {
         __syncthreads();                       // the previous piece's reads of sel/piece are done
         if (t == 0) {

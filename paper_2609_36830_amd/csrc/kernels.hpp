@@ -120,6 +120,14 @@ struct CutRec {
     int64_t pad;
 };
 constexpr int kWideBlock = 64;          // trajectories per compaction block on the wide path
+// Pieces of a wide block: each kept span longer than kPieceLen is cut into
+// ceil(len / kPieceLen) pieces; the shorter kept spans, taken together in
+// block order, into segments of kSegLen tokens (the last one shorter), of
+// which the block's own workgroup copies the first.
+constexpr int64_t kSegLen = 24576;
+__host__ __device__ inline int64_t wide_block_pieces(int64_t long_pieces, int64_t short_tokens) {
+    return long_pieces + (short_tokens > 0 ? (short_tokens - 1) / kSegLen : 0);
+}
 constexpr int64_t kWideHistMax = 64;    // histogram workgroups
 constexpr int64_t kWideMaxN = 262144;   // piece compaction limit with wide blocks
 struct WideWs {

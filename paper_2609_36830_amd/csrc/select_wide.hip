@@ -340,8 +340,8 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
 
 // One thread per trajectory: the keep flag from the cut; then the partials
 // of each block of kWideBlock trajectories (one wave): kept count, kept
-// tokens (spans clamped to [0, NT]) and pieces of at most kPieceLen tokens
-// (zero without offsets).
+// tokens (spans clamped to [0, NT]) and pieces (wide_block_pieces; zero
+// without offsets).
 __global__ __launch_bounds__(256) void classify_kernel(const double *__restrict__ score,
                                                        const int64_t *__restrict__ off, int64_t n, int64_t NT,
                                                        const CutRec *__restrict__ cut_p, uint8_t *__restrict__ keep,
@@ -364,7 +364,8 @@ __global__ __launch_bounds__(256) void classify_kernel(const double *__restrict_
     }
     const uint32_t kc = (uint32_t)__popcll(ballot(kept));
     const int64_t l = wave_sum_i64(len);
-    const int64_t pc = wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
+    const int64_t pc = wide_block_pieces(wave_sum_i64(len > kPieceLen ? (len + kPieceLen - 1) / kPieceLen : 0),
+                                         wave_sum_i64(len > kPieceLen ? 0 : len));
     const int64_t b = i / kWideBlock;
     if (lane_id() == 0 && b * kWideBlock < n) {
         parts.cnt[b] = (int32_t)kc;
