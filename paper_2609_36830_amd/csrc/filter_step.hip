@@ -51,7 +51,8 @@ hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64
     if (e != hipSuccess) return e;
     e = launch_score_finalize(offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix,
                               w_wait, gamma, chunk_len, score, gen_sum, gen_count, sws, stream,
-                              wide_path ? ww.mmin : nullptr, wide_path ? ww.mmax : nullptr);
+                              wide_path ? ww.mmin : nullptr, wide_path ? ww.mmax : nullptr,
+                              wide_path ? ww.hist : nullptr);
     if (e != hipSuccess) return e;
     if (wide_path) {
         const CompactWs cw = compact_ws_carve(cws_base, n, n_tokens);

@@ -76,14 +76,16 @@ hipError_t launch_score_reduce(const int32_t *tags, const int64_t *offsets, int6
                                int64_t n_tokens, int32_t V, const ScoreWorkspace &ws, bool vec_ok,
                                hipStream_t stream, int64_t *chunk_len_out);
 // With mmin/mmax non-null, also writes the smallest and largest score key
-// of each group of kFinGroup trajectories (the wide selection's range).
+// of each group of kFinGroup trajectories (the wide selection's range) and
+// clears hist0 (2^kCutBits words, the wide selection's level-0 histogram).
 constexpr int kFinGroup = 128;
 hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_tokens,
                                  const int32_t *completion, int32_t V, const double *prefix,
                                  const double *window, int64_t W, bool use_prefix, double w_wait,
                                  int gamma, int64_t chunk_len, double *score, int64_t *gen_sum,
                                  int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream,
-                                 uint64_t *mmin = nullptr, uint64_t *mmax = nullptr);
+                                 uint64_t *mmin = nullptr, uint64_t *mmax = nullptr,
+                                 uint32_t *hist0 = nullptr);
 hipError_t launch_score(const int32_t *tags, const int64_t *offsets, int64_t n, int64_t n_tokens,
                         const int32_t *completion, int32_t V, const double *prefix,
                         const double *window, int64_t W, bool use_prefix, double w_wait, int gamma,
@@ -130,11 +132,13 @@ __host__ __device__ inline int64_t wide_block_pieces(int64_t long_pieces, int64_
 }
 constexpr int64_t kWideHistMax = 64;    // histogram workgroups
 constexpr int64_t kWideMaxN = 262144;   // piece compaction limit with wide blocks
+constexpr int kCutBits = 11;           // level-0 digits of the cut search: 2^kCutBits bins
 struct WideWs {
     CutRec *cut;
     uint64_t *range;
     uint64_t *mmin, *mmax;   // [n_mm] per group of kFinGroup trajectories
-    uint32_t *hist;          // [kWideHistMax][bins]
+    uint32_t *hist;          // [2^kCutBits] level-0 histogram, cleared by the kernel writing mmin/mmax
+    uint16_t *digit;         // [n] level-0 digit of each trajectory
     PieceParts parts;        // [n / kWideBlock] partials when no compaction workspace is at hand
     int64_t n_mm;
 };

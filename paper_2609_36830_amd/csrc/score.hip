@@ -346,14 +346,15 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
 constexpr int kFinT = kFinGroup;
 
 // kMinMax: the workgroup also writes the smallest and largest score key of
-// its trajectories (mmin, mmax), the range the wide selection histograms.
+// its trajectories (mmin, mmax), the range the wide selection histograms;
+// workgroup 0 clears that selection's level-0 histogram (hist0).
 template <bool kWinLds, bool kMinMax>
 __global__ __launch_bounds__(kFinT) void score_finalize_kernel(
     const int64_t *__restrict__ off, int64_t n, int64_t NT, const int32_t *__restrict__ completion,
     int32_t V, const double *__restrict__ prefix, const double *__restrict__ window, int64_t W,
     int use_prefix, double w_wait, int gamma, int64_t chunk_len, ScoreWorkspace ws,
     double *__restrict__ score, int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count,
-    uint64_t *__restrict__ mmin, uint64_t *__restrict__ mmax) {
+    uint64_t *__restrict__ mmin, uint64_t *__restrict__ mmax, uint32_t *__restrict__ hist0) {
     __shared__ double win_lds[kWinLds ? kWindowLdsMax : 1];
     const bool narrow = (NT >> 11) < ((int64_t)1 << 32);   // token positions below 2^43
     // The trajectory's own loads go first (they do not wait for the window),
@@ -389,6 +390,8 @@ __global__ __launch_bounds__(kFinT) void score_finalize_kernel(
         key = score_key(r.score);
     }
     if constexpr (kMinMax) {
+        if (blockIdx.x == 0)
+            for (int b = threadIdx.x; b < (1 << kCutBits); b += kFinT) hist0[b] = 0u;
         __shared__ uint64_t wl[kFinT / kWave], wh[kFinT / kWave];
         const uint64_t lo = wave_min_u64(in ? key : ~0ull), hi = wave_max_u64(key);
         if (lane_id() == 0) {
@@ -453,14 +456,14 @@ hipError_t launch_score_finalize(const int64_t *offsets, int64_t n, int64_t n_to
                                  const double *window, int64_t W, bool use_prefix, double w_wait,
                                  int gamma, int64_t chunk_len, double *score, int64_t *gen_sum,
                                  int64_t *gen_count, const ScoreWorkspace &ws, hipStream_t stream,
-                                 uint64_t *mmin, uint64_t *mmax) {
+                                 uint64_t *mmin, uint64_t *mmax, uint32_t *hist0) {
     if (n == 0) return hipSuccess;
     const unsigned grid = (unsigned)((n + kFinT - 1) / kFinT);
     const bool win_lds = use_prefix && W <= kWindowLdsMax;
 #define PACE_FIN(WIN, MM)                                                                                    \
     return launch(kPhaseFinalize, score_finalize_kernel<WIN, MM>, dim3(grid), dim3(kFinT), stream, offsets, n, \
                   n_tokens, completion, V, prefix, window, W, use_prefix ? 1 : 0, w_wait, gamma, chunk_len, ws,   \
-                  score, gen_sum, gen_count, mmin, mmax)
+                  score, gen_sum, gen_count, mmin, mmax, hist0)
     if (mmin) {
         if (win_lds) PACE_FIN(true, true);
         PACE_FIN(false, true);

@@ -8,24 +8,27 @@
 //   key_minmax  (only when the scores do not come from the filter step's
 //               finalize, which writes the same per-group minima and maxima)
 //               per group of trajectories, the smallest and largest key;
-//   cut_hist    up to kWideHistMax workgroups: the global key range [lo, hi] from the
-//               group extremes, then each workgroup histograms its slice of
-//               the keys into kHBins bins of 2^shift keys, (key - lo) >>
-//               shift (monotone in the key), and writes its histogram;
-//   cut_select  one workgroup: sums the histograms and scans the bins from
-//               the top for the bin holding the budget-th largest key. Its
-//               keys (the candidates) are staged in LDS with one pass over
-//               the scores when they fit, and the same bin search repeats on
-//               them with finer bins until at most kPair remain, which are
-//               ranked pairwise by (key desc, id asc). A bin rejected whole
-//               ends the search early; equal keys are ordered by id with an
-//               ordered count. More candidates than LDS holds are refined by
-//               histogramming the scores again from global memory.
+//               workgroup 0 clears the level-0 histogram;
+//   cut_hist    up to kWideHistMax workgroups: the global key range [lo, hi]
+//               from the group extremes, then each workgroup takes the
+//               level-0 digit (Level0: linear in the score when the range is
+//               finite, else the top bits of key - lo; monotone in the key)
+//               of every score in its slice, keeps it (16 bits per
+//               trajectory) and adds its LDS histogram to the global one;
+//   cut_select  one workgroup: scans the global histogram from the top for
+//               the bin holding the budget-th largest key; stages that bin's
+//               keys (candidates) in LDS with one pass over the digits when
+//               they fit, and repeats the bin search on them with finer key
+//               bins until at most kPair remain, which are ranked pairwise by
+//               (key desc, id asc). A bin rejected whole ends the search
+//               early; equal keys are ordered by id with an ordered count.
+//               More candidates than LDS holds are refined by histogramming
+//               the scores again from global memory.
 //   classify    one thread per trajectory applies the cut: keep flags, and
 //               per block of kWideBlock trajectories the kept count, kept
 //               tokens and piece count the piece compaction consumes.
-// Every histogram uses LDS atomics on few keys per workgroup, and no kernel
-// needs zeroed memory or an atomic in global memory.
+// Histograms use LDS atomics, plus one global atomic per non-empty bin and
+// workgroup; the integer counts do not depend on their order.
 #include "device_util.hpp"
 #include "kernels.hpp"
 
@@ -33,7 +36,7 @@ namespace pace {
 
 namespace {
 
-constexpr int kHBits = 11;
+constexpr int kHBits = kCutBits;
 constexpr int kHBins = 1 << kHBits;
 constexpr int kWT = 1024;                // threads of the histogram and cut workgroups
 constexpr int kWW = kWT / kWave;
@@ -57,10 +60,52 @@ __device__ __forceinline__ bool cut_rejects(const CutRec &c, uint64_t k, int64_t
     }
 }
 
+// The score of a key (inverse of score_key; NaN for the NaN key).
+__device__ __forceinline__ double key_score(uint64_t k) {
+    const uint64_t b = (k >> 63) ? (k & 0x7fffffffffffffffull) : ~k;
+    return __longlong_as_double((long long)b);
+}
+
+// Level-0 digit: linear in the score over [smin, smax] when both ends and
+// their difference are finite and the range is not a point (bins of equal
+// score width: a score distribution spreads over many of them), else the top
+// bits of key - lo (bins of equal key width, which for binary64 keys mostly
+// separate exponents). Either way the digit is monotone in the key, so every
+// bin holds a contiguous range of keys.
+struct Level0 {
+    bool linear;
+    double smin, scale;
+    uint64_t lo;
+    int sh;
+    __device__ __forceinline__ uint32_t digit(uint64_t key, double s) const {
+        if (linear) {
+            const double x = (s - smin) * scale;
+            return x < (double)(kHBins - 1) ? (uint32_t)x : (uint32_t)(kHBins - 1);
+        }
+        const uint64_t d = (key - lo) >> sh;
+        return d < (uint64_t)kHBins ? (uint32_t)d : (uint32_t)(kHBins - 1);
+    }
+};
+__device__ __forceinline__ Level0 level0(uint64_t lo, uint64_t hi) {
+    Level0 L;
+    const double a = key_score(lo), b = key_score(hi);
+    const double w = b - a;
+    L.linear = __builtin_isfinite(a) && __builtin_isfinite(b) && __builtin_isfinite(w) && w > 0.0;
+    L.smin = a;
+    L.scale = L.linear ? (double)kHBins / w : 0.0;
+    L.lo = lo;
+    L.sh = range_shift(lo, hi);
+    return L;
+}
+
 // Smallest and largest key of each group of kMMT scores.
+// Workgroup 0 also clears the level-0 histogram.
 __global__ __launch_bounds__(kMMT) void key_minmax_kernel(const double *__restrict__ score, int64_t n,
-                                                          uint64_t *__restrict__ mmin, uint64_t *__restrict__ mmax) {
+                                                          uint64_t *__restrict__ mmin, uint64_t *__restrict__ mmax,
+                                                          uint32_t *__restrict__ hist0) {
     __shared__ uint64_t wl[kMMT / kWave], wh[kMMT / kWave];
+    if (blockIdx.x == 0)
+        for (int b = threadIdx.x; b < kHBins; b += kMMT) hist0[b] = 0u;
     const int64_t i = (int64_t)blockIdx.x * kMMT + threadIdx.x;
     const uint64_t k = i < n ? score_key(score[i]) : 0ull;
     const uint64_t lo = wave_min_u64(i < n ? k : ~0ull), hi = wave_max_u64(k);
@@ -80,16 +125,27 @@ __global__ __launch_bounds__(kMMT) void key_minmax_kernel(const double *__restri
     }
 }
 
+// Each workgroup histograms the level-0 digits of its slice of the scores in
+// LDS, keeps every digit (16 bits per trajectory, for the cut workgroup's
+// staging pass) and adds its non-empty bins to the global histogram, which the
+// kernel before it cleared.
 __global__ __launch_bounds__(kWT) void cut_hist_kernel(const double *__restrict__ score, int64_t n,
                                                        const uint64_t *__restrict__ mmin,
                                                        const uint64_t *__restrict__ mmax, int64_t n_mm,
                                                        int64_t per_wg, uint32_t *__restrict__ hist,
-                                                       uint64_t *__restrict__ range) {
+                                                       uint16_t *__restrict__ digit, uint64_t *__restrict__ range) {
     __shared__ uint32_t h[kHBins];
     __shared__ uint64_t wl[kWW], wh[kWW];
     const int t = threadIdx.x, lane = lane_id(), wv = t / kWave;
     const int64_t i0 = (int64_t)blockIdx.x * per_wg;
     const int64_t i1 = (i0 + per_wg < n) ? i0 + per_wg : n;
+    // The first scores of the slice do not depend on the range: load them first.
+    double sc[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int64_t j = i0 + t + (int64_t)u * kWT;
+        sc[u] = j < i1 ? score[j] : 0.0;
+    }
     for (int b = t; b < kHBins; b += kWT) h[b] = 0u;
     uint64_t lo = ~0ull, hi = 0;
     for (int64_t i = t; i < n_mm; i += kWT) {
@@ -111,24 +167,28 @@ __global__ __launch_bounds__(kWT) void cut_hist_kernel(const double *__restrict_
         lo = wl[w] < lo ? wl[w] : lo;
         hi = wh[w] > hi ? wh[w] : hi;
     }
-    const int sh = range_shift(lo, hi);
+    const Level0 L = level0(lo, hi);
     for (int64_t i = i0 + t; i < i1; i += 4 * kWT) {
-        uint64_t k[4];
+        if (i != i0 + t) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int64_t j = i + (int64_t)u * kWT;
-            k[u] = j < i1 ? score_key(score[j]) : 0ull;
+            for (int u = 0; u < 4; ++u) {
+                const int64_t j = i + (int64_t)u * kWT;
+                sc[u] = j < i1 ? score[j] : 0.0;
+            }
         }
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            if (i + (int64_t)u * kWT < i1) {
-                const uint64_t d = (k[u] - lo) >> sh;     // below kHBins for keys in [lo, hi]
-                atomicAdd(&h[d < (uint64_t)kHBins ? d : (uint64_t)kHBins - 1], 1u);
+            const int64_t j = i + (int64_t)u * kWT;
+            if (j < i1) {
+                const uint32_t d = L.digit(score_key(sc[u]), sc[u]);
+                atomicAdd(&h[d], 1u);
+                digit[j] = (uint16_t)d;
             }
         }
     }
     __syncthreads();
-    for (int b = t; b < kHBins; b += kWT) hist[(int64_t)blockIdx.x * kHBins + b] = h[b];
+    for (int b = t; b < kHBins; b += kWT)
+        if (h[b] != 0u) atomicAdd(&hist[b], h[b]);
     if (blockIdx.x == 0 && t == 0) {
         range[0] = lo;
         range[1] = hi;
@@ -137,7 +197,8 @@ __global__ __launch_bounds__(kWT) void cut_hist_kernel(const double *__restrict_
 
 __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restrict__ score, int64_t n,
                                                          int64_t budget, const uint32_t *__restrict__ hist,
-                                                         int64_t n_hist, const uint64_t *__restrict__ range,
+                                                         const uint16_t *__restrict__ digit,
+                                                         const uint64_t *__restrict__ range,
                                                          CutRec *__restrict__ out) {
     __shared__ uint32_t h[kHBins];
     __shared__ uint32_t wsum[kWW];
@@ -146,7 +207,8 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
     __shared__ uint32_t ncand;
     __shared__ uint64_t s_lo, s_hi, s_key;
     __shared__ int64_t s_need, s_id;
-    __shared__ uint32_t s_cnt;
+    __shared__ uint32_t s_cnt, s_d;
+    __shared__ uint64_t wl[kWW], wh[kWW];
     const int t = threadIdx.x, lane = lane_id();
     if (budget <= 0 || budget >= n) {
         if (t == 0) *out = CutRec{budget <= 0 ? 0 : 1, 0, 0, 0};
@@ -183,24 +245,108 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
         if (t == 0) *out = CutRec{2, lo, 0, 0};
     };
 
-    // Level 0: the workgroup histograms.
+    // Level 0: the global histogram of the level-0 digits, from the top.
+    uint32_t d0;
     {
-        const int sh = range_shift(lo, hi);
-        uint32_t a = 0, b = 0;
-        for (int64_t g = 0; g < n_hist; ++g) {
-            a += hist[g * kHBins + (kHBins - 1 - 2 * t)];
-            b += hist[g * kHBins + (kHBins - 2 - 2 * t)];
+        uint32_t tot;
+        const uint32_t a = hist[kHBins - 1 - 2 * t], b = hist[kHBins - 2 - 2 * t];
+        const uint32_t ex = block_excl_sum_u32<kWW>(a + b, tot, wsum);
+        if ((int64_t)ex < need && need <= (int64_t)ex + a + b) {
+            const bool first = need <= (int64_t)ex + a;
+            s_d = first ? (uint32_t)(kHBins - 1 - 2 * t) : (uint32_t)(kHBins - 2 - 2 * t);
+            s_need = need - (int64_t)(first ? ex : ex + a);
+            s_cnt = first ? a : b;
         }
-        pick(a, b, sh);
-        if (need == (int64_t)cnt) {
-            reject_bin_and_above();
-            return;
+        __syncthreads();
+        d0 = s_d;
+        need = s_need;
+        cnt = s_cnt;
+        __syncthreads();
+    }
+    // The keys of bin d0: staged in LDS when they fit (a pass over the
+    // digits, then one load of each candidate's score), else only their
+    // smallest and largest key. Either way [lo, hi] becomes the bin's key
+    // range.
+    bool staged = false;
+    if (cnt <= (uint32_t)kCandCap) {
+        if (t == 0) ncand = 0u;
+        __syncthreads();
+        constexpr int kDU = 8;                   // 16-byte digit vectors in flight per thread
+        const int64_t nv = (n + 7) / 8;
+        for (int64_t v0 = t; v0 < nv; v0 += (int64_t)kDU * kWT) {
+            uint4 dv[kDU];
+#pragma unroll
+            for (int u = 0; u < kDU; ++u) {
+                const int64_t v = v0 + (int64_t)u * kWT;
+                dv[u] = v < nv ? *reinterpret_cast<const uint4 *>(digit + v * 8) : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int u = 0; u < kDU; ++u) {
+                const int64_t v = v0 + (int64_t)u * kWT;
+                const uint32_t wd[4] = {dv[u].x, dv[u].y, dv[u].z, dv[u].w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int64_t i = v * 8 + e;
+                    const bool c = v < nv && i < n && ((wd[e >> 1] >> (16 * (e & 1))) & 0xffffu) == d0;
+                    const uint64_t m = ballot(c);
+                    if (m != 0ull) {
+                        const int leader = __ffsll((long long)m) - 1;
+                        uint32_t base = 0;
+                        if (lane == leader) base = atomicAdd(&ncand, (uint32_t)__popcll(m));
+                        base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
+                        const uint32_t sl = base + (uint32_t)__popcll(m & lanes_below());
+                        if (c && sl < (uint32_t)kCandCap) ci[sl] = (uint32_t)i;
+                    }
+                }
+            }
         }
+        __syncthreads();
+        cnt = ncand < (uint32_t)kCandCap ? ncand : (uint32_t)kCandCap;
+        uint64_t kl = ~0ull, kh = 0;
+        for (uint32_t j = (uint32_t)t; j < cnt; j += kWT) {
+            const uint64_t k = score_key(score[ci[j]]);
+            ck[j] = k;
+            kl = k < kl ? k : kl;
+            kh = k > kh ? k : kh;
+        }
+        kl = wave_min_u64(kl);
+        kh = wave_max_u64(kh);
+        if (lane == 0) {
+            wl[t / kWave] = kl;
+            wh[t / kWave] = kh;
+        }
+        staged = true;
+    } else {
+        uint64_t kl = ~0ull, kh = 0;
+        for (int64_t i = t; i < n; i += kWT) {
+            if (digit[i] == d0) {
+                const uint64_t k = score_key(score[i]);
+                kl = k < kl ? k : kl;
+                kh = k > kh ? k : kh;
+            }
+        }
+        kl = wave_min_u64(kl);
+        kh = wave_max_u64(kh);
+        if (lane == 0) {
+            wl[t / kWave] = kl;
+            wh[t / kWave] = kh;
+        }
+    }
+    __syncthreads();
+    lo = ~0ull;
+    hi = 0;
+#pragma unroll
+    for (int w = 0; w < kWW; ++w) {
+        lo = wl[w] < lo ? wl[w] : lo;
+        hi = wh[w] > hi ? wh[w] : hi;
+    }
+    if (need == (int64_t)cnt) {
+        reject_bin_and_above();
+        return;
     }
 
     // Finer levels until at most kPair candidates remain or they all share
     // one key (each level splits the key range by 2^kHBits, so six suffice).
-    bool staged = false;
     for (int level = 0; level < 8 && lo != hi; ++level) {
         if (!staged && cnt <= (uint32_t)kCandCap) {
             // One pass over the scores stages every key in [lo, hi].
@@ -401,7 +547,7 @@ int64_t wide_hist_wgs(int64_t n) {
 size_t wide_select_ws_bytes(int64_t n) {
     const int64_t mm = (n + kMMT - 1) / kMMT;
     const int64_t nb = (n + kWideBlock - 1) / kWideBlock;
-    return 256 + align256((size_t)mm * 8) * 2 + align256((size_t)kWideHistMax * kHBins * 4) +
+    return 256 + align256((size_t)mm * 8) * 2 + align256((size_t)kHBins * 4) + align256((size_t)n * 2) +
            align256((size_t)nb * 4) * 2 + align256((size_t)nb * 8);
 }
 
@@ -413,7 +559,8 @@ WideWs wide_ws_carve(void *ws, int64_t n) {
     w.range = (uint64_t *)p;    p += 192;
     w.mmin = (uint64_t *)p;     p += align256((size_t)mm * 8);
     w.mmax = (uint64_t *)p;     p += align256((size_t)mm * 8);
-    w.hist = (uint32_t *)p;     p += align256((size_t)kWideHistMax * kHBins * 4);
+    w.hist = (uint32_t *)p;     p += align256((size_t)kHBins * 4);
+    w.digit = (uint16_t *)p;    p += align256((size_t)n * 2);
     const int64_t nb = (n + kWideBlock - 1) / kWideBlock;
     w.parts.cnt = (int32_t *)p; p += align256((size_t)nb * 4);
     w.parts.len = (int64_t *)p; p += align256((size_t)nb * 8);
@@ -425,7 +572,7 @@ WideWs wide_ws_carve(void *ws, int64_t n) {
 hipError_t launch_key_minmax(const double *score, int64_t n, const WideWs &w, hipStream_t stream) {
     if (n == 0) return hipSuccess;
     return launch(kPhaseSelect, key_minmax_kernel, dim3((unsigned)w.n_mm), dim3(kMMT), stream, score, n, w.mmin,
-                  w.mmax);
+                  w.mmax, w.hist);
 }
 
 hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const WideWs &w, hipStream_t stream) {
@@ -433,9 +580,9 @@ hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const
     const int64_t g = wide_hist_wgs(n);
     const int64_t per = (n + g - 1) / g;
     hipError_t e = launch(kPhaseSelect, cut_hist_kernel, dim3((unsigned)g), dim3(kWT), stream, score, n, w.mmin,
-                          w.mmax, w.n_mm, per, w.hist, w.range);
+                          w.mmax, w.n_mm, per, w.hist, w.digit, w.range);
     if (e != hipSuccess) return e;
-    return launch(kPhaseSelect, cut_select_kernel, dim3(1), dim3(kWT), stream, score, n, budget, w.hist, g,
+    return launch(kPhaseSelect, cut_select_kernel, dim3(1), dim3(kWT), stream, score, n, budget, w.hist, w.digit,
                   w.range, w.cut);
 }
 
