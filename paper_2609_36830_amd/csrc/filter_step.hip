@@ -58,7 +58,7 @@ hipError_t launch_filter_step(const int32_t *tags, const int64_t *offsets, int64
         const CompactWs cw = compact_ws_carve(cws_base, n, n_tokens);
         e = launch_wide_cut(score, n, budget, ww, stream);
         if (e != hipSuccess) return e;
-        e = launch_classify(score, offsets, n, n_tokens, ww, keep, cw.parts, stream);
+        e = launch_classify(score, offsets, n, n_tokens, budget, ww, keep, cw.parts, stream);
         if (e != hipSuccess) return e;
         const int64_t n_kept = n - (budget < n ? budget : n);
         return launch_compact_pieces(offsets, n, n_tokens, keep, cw.parts, cols, n_cols, offsets_out,

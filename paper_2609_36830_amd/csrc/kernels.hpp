@@ -146,6 +146,8 @@ int64_t wide_hist_wgs(int64_t n);
 size_t wide_select_ws_bytes(int64_t n);
 WideWs wide_ws_carve(void *ws, int64_t n);
 hipError_t launch_key_minmax(const double *score, int64_t n, const WideWs &w, hipStream_t stream);
+// The level-0 digits and histogram of the cut search (after the kernel that
+// writes mmin/mmax and clears hist).
 hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const WideWs &w, hipStream_t stream);
 
 // keep[i] <- 0 for the `budget` first trajectories in (score desc, id asc).
@@ -154,9 +156,13 @@ hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *
                        const int64_t *offsets, int64_t n_tokens, const PieceParts &parts,
                        hipStream_t stream);
 size_t select_ws_bytes(int64_t n);
-// offsets may be null (keep flags and kept counts only).
+// Every workgroup finds the cut of the `budget` highest from the level-0
+// histogram and digits, then classifies its trajectories (keep flags, block
+// partials; offsets may be null: keep flags and kept counts only); w.cut
+// receives the cut.
 hipError_t launch_classify(const double *score, const int64_t *offsets, int64_t n, int64_t n_tokens,
-                           const WideWs &w, uint8_t *keep, const PieceParts &parts, hipStream_t stream);
+                           int64_t budget, const WideWs &w, uint8_t *keep, const PieceParts &parts,
+                           hipStream_t stream);
 hipError_t launch_emit_rejects_wide(const uint8_t *keep, int64_t n, const int32_t *kept_cnt, int64_t budget,
                                     int32_t *reject_ids, hipStream_t stream);
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,

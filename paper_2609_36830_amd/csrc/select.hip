@@ -414,7 +414,7 @@ hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t
         const WideWs w = wide_ws_carve(ws, n);
         hipError_t e = launch_key_minmax(score, n, w, stream);
         if (e == hipSuccess) e = launch_wide_cut(score, n, budget, w, stream);
-        if (e == hipSuccess) e = launch_classify(score, nullptr, n, 0, w, keep, w.parts, stream);
+        if (e == hipSuccess) e = launch_classify(score, nullptr, n, 0, budget, w, keep, w.parts, stream);
         if (e == hipSuccess) e = launch_emit_rejects_wide(keep, n, w.parts.cnt, budget, reject_ids, stream);
         return e;
     }

@@ -15,17 +15,18 @@
 //               finite, else the top bits of key - lo; monotone in the key)
 //               of every score in its slice, keeps it (16 bits per
 //               trajectory) and adds its LDS histogram to the global one;
-//   cut_select  one workgroup: scans the global histogram from the top for
+//   classify    1024-thread workgroups; each first finds the cut itself
+//               (find_cut): scans the global histogram from the top for
 //               the bin holding the budget-th largest key; stages that bin's
 //               keys (candidates) in LDS with one pass over the digits when
 //               they fit, and repeats the bin search on them with finer key
-//               bins until at most kPair remain, which are ranked pairwise by
-//               (key desc, id asc). A bin rejected whole ends the search
-//               early; equal keys are ordered by id with an ordered count.
-//               More candidates than LDS holds are refined by histogramming
-//               the scores again from global memory.
-//   classify    one thread per trajectory applies the cut: keep flags, and
-//               per block of kWideBlock trajectories the kept count, kept
+//               bins until at most kRankMax remain, which are ranked by
+//               counting on (key desc, id asc). A bin rejected whole ends the
+//               search early; many equal keys are ordered by id with an
+//               ordered count. More candidates than LDS holds are refined by
+//               histogramming the scores again from global memory.
+//               Then one thread per trajectory applies the cut: keep flags,
+//               and per block of kWideBlock trajectories the kept count, kept
 //               tokens and piece count the piece compaction consumes.
 // Histograms use LDS atomics, plus one global atomic per non-empty bin and
 // workgroup; the integer counts do not depend on their order.
@@ -41,7 +42,6 @@ constexpr int kHBins = 1 << kHBits;
 constexpr int kWT = 1024;                // threads of the histogram and cut workgroups
 constexpr int kWW = kWT / kWave;
 constexpr int kCandCap = 4096;           // candidates staged in LDS
-constexpr int kPair = 64;                // candidates ranked pairwise (one wave)
 constexpr int kMMT = kFinGroup;          // threads of a min/max workgroup (one key each)
 
 // Bins of 2^shift keys cover [lo, hi] in at most kHBins bins.
@@ -195,54 +195,61 @@ __global__ __launch_bounds__(kWT) void cut_hist_kernel(const double *__restrict_
     }
 }
 
-__global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restrict__ score, int64_t n,
-                                                         int64_t budget, const uint32_t *__restrict__ hist,
-                                                         const uint16_t *__restrict__ digit,
-                                                         const uint64_t *__restrict__ range,
-                                                         CutRec *__restrict__ out) {
-    __shared__ uint32_t h[kHBins];
-    __shared__ uint32_t wsum[kWW];
-    __shared__ uint64_t ck[kCandCap];
-    __shared__ uint32_t ci[kCandCap];
-    __shared__ uint32_t ncand;
-    __shared__ uint64_t s_lo, s_hi, s_key;
-    __shared__ int64_t s_need, s_id;
-    __shared__ uint32_t s_cnt, s_d;
-    __shared__ uint64_t wl[kWW], wh[kWW];
+// Shared memory of the cut search (one 1024-thread workgroup).
+struct CutSmem {
+    uint32_t h[kHBins];
+    uint32_t wsum[kWW];
+    uint64_t ck[kCandCap];
+    uint32_t ci[kCandCap];
+    uint32_t ncand;
+    uint64_t s_lo, s_hi, s_key;
+    int64_t s_need, s_id;
+    uint32_t s_cnt, s_d;
+    uint64_t wl[kWW], wh[kWW];
+    CutRec cut;
+};
+constexpr int kRankMax = kWT / 4;        // candidates ranked by counting, four threads each
+
+// The rejection cut of the budget highest (key, -id) from the level-0
+// histogram and digits. Called by every thread of a kWT-thread workgroup; the
+// result is in sm.cut after the caller's next barrier.
+__device__ void find_cut(const double *__restrict__ score, int64_t n, int64_t budget,
+                         const uint32_t *__restrict__ hist, const uint16_t *__restrict__ digit,
+                         const uint64_t *__restrict__ range, CutSmem &sm) {
     const int t = threadIdx.x, lane = lane_id();
     if (budget <= 0 || budget >= n) {
-        if (t == 0) *out = CutRec{budget <= 0 ? 0 : 1, 0, 0, 0};
+        if (t == 0) sm.cut = CutRec{budget <= 0 ? 0 : 1, 0, 0, 0};
         return;
     }
     uint64_t lo = range[0], hi = range[1];
     int64_t need = budget;
     uint32_t cnt = 0;
 
-    // Descending bin search: thread t holds the counts a, b of digits
-    // kHBins - 1 - 2t and kHBins - 2 - 2t. Narrows [lo, hi] to the bin that
-    // holds the need-th largest candidate.
+    // Descending bin search over key bins of 2^sh: thread t holds the counts
+    // a, b of digits kHBins - 1 - 2t and kHBins - 2 - 2t. Narrows [lo, hi] to
+    // the bin that holds the need-th largest candidate.
     auto pick = [&](uint32_t a, uint32_t b, int sh) {
         uint32_t tot;
-        const uint32_t ex = block_excl_sum_u32<kWW>(a + b, tot, wsum);
+        const uint32_t ex = block_excl_sum_u32<kWW>(a + b, tot, sm.wsum);
         if ((int64_t)ex < need && need <= (int64_t)ex + a + b) {
             const bool first = need <= (int64_t)ex + a;
             const uint64_t d = first ? (uint64_t)(kHBins - 1 - 2 * t) : (uint64_t)(kHBins - 2 - 2 * t);
             const uint64_t blo = lo + (d << sh);
             const uint64_t room = hi - blo, w = (((uint64_t)1 << sh) - 1);
-            s_need = need - (int64_t)(first ? ex : ex + a);
-            s_cnt = first ? a : b;
-            s_lo = blo;
-            s_hi = blo + (room < w ? room : w);
+            sm.s_need = need - (int64_t)(first ? ex : ex + a);
+            sm.s_cnt = first ? a : b;
+            sm.s_lo = blo;
+            sm.s_hi = blo + (room < w ? room : w);
         }
         __syncthreads();
-        need = s_need;
-        cnt = s_cnt;
-        lo = s_lo;
-        hi = s_hi;
+        need = sm.s_need;
+        cnt = sm.s_cnt;
+        lo = sm.s_lo;
+        hi = sm.s_hi;
         __syncthreads();
     };
     auto reject_bin_and_above = [&]() {
-        if (t == 0) *out = CutRec{2, lo, 0, 0};
+        if (t == 0) sm.cut = CutRec{2, lo, 0, 0};
     };
 
     // Level 0: the global histogram of the level-0 digits, from the top.
@@ -250,17 +257,18 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
     {
         uint32_t tot;
         const uint32_t a = hist[kHBins - 1 - 2 * t], b = hist[kHBins - 2 - 2 * t];
-        const uint32_t ex = block_excl_sum_u32<kWW>(a + b, tot, wsum);
+        const uint32_t ex = block_excl_sum_u32<kWW>(a + b, tot, sm.wsum);
         if ((int64_t)ex < need && need <= (int64_t)ex + a + b) {
             const bool first = need <= (int64_t)ex + a;
-            s_d = first ? (uint32_t)(kHBins - 1 - 2 * t) : (uint32_t)(kHBins - 2 - 2 * t);
-            s_need = need - (int64_t)(first ? ex : ex + a);
-            s_cnt = first ? a : b;
+            sm.s_d = first ? (uint32_t)(kHBins - 1 - 2 * t) : (uint32_t)(kHBins - 2 - 2 * t);
+            sm.s_need = need - (int64_t)(first ? ex : ex + a);
+            sm.s_cnt = first ? a : b;
         }
+        if (t == 0) sm.ncand = 0u;
         __syncthreads();
-        d0 = s_d;
-        need = s_need;
-        cnt = s_cnt;
+        d0 = sm.s_d;
+        need = sm.s_need;
+        cnt = sm.s_cnt;
         __syncthreads();
     }
     // The keys of bin d0: staged in LDS when they fit (a pass over the
@@ -268,56 +276,50 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
     // smallest and largest key. Either way [lo, hi] becomes the bin's key
     // range.
     bool staged = false;
+    uint64_t kl = ~0ull, kh = 0;
     if (cnt <= (uint32_t)kCandCap) {
-        if (t == 0) ncand = 0u;
-        __syncthreads();
         constexpr int kDU = 8;                   // 16-byte digit vectors in flight per thread
         const int64_t nv = (n + 7) / 8;
+        const uint32_t dd = d0 | (d0 << 16);
         for (int64_t v0 = t; v0 < nv; v0 += (int64_t)kDU * kWT) {
             uint4 dv[kDU];
 #pragma unroll
             for (int u = 0; u < kDU; ++u) {
                 const int64_t v = v0 + (int64_t)u * kWT;
-                dv[u] = v < nv ? *reinterpret_cast<const uint4 *>(digit + v * 8) : make_uint4(0, 0, 0, 0);
+                dv[u] = v < nv ? *reinterpret_cast<const uint4 *>(digit + v * 8) : make_uint4(~0u, ~0u, ~0u, ~0u);
             }
 #pragma unroll
             for (int u = 0; u < kDU; ++u) {
-                const int64_t v = v0 + (int64_t)u * kWT;
-                const uint32_t wd[4] = {dv[u].x, dv[u].y, dv[u].z, dv[u].w};
+                // Digits are below 2^15, so (x - 0x10001) & ~x & 0x80008000 is
+                // non-zero exactly when a half of x = word ^ dd is zero (or
+                // the borrow of a zero low half reaches the high one).
+                const uint32_t wd[4] = {dv[u].x ^ dd, dv[u].y ^ dd, dv[u].z ^ dd, dv[u].w ^ dd};
+                uint32_t any = 0;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int64_t i = v * 8 + e;
-                    const bool c = v < nv && i < n && ((wd[e >> 1] >> (16 * (e & 1))) & 0xffffu) == d0;
-                    const uint64_t m = ballot(c);
-                    if (m != 0ull) {
-                        const int leader = __ffsll((long long)m) - 1;
-                        uint32_t base = 0;
-                        if (lane == leader) base = atomicAdd(&ncand, (uint32_t)__popcll(m));
-                        base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
-                        const uint32_t sl = base + (uint32_t)__popcll(m & lanes_below());
-                        if (c && sl < (uint32_t)kCandCap) ci[sl] = (uint32_t)i;
+                for (int e = 0; e < 4; ++e) any |= (wd[e] - 0x00010001u) & ~wd[e] & 0x80008000u;
+                if (any != 0u) {
+                    const int64_t v = v0 + (int64_t)u * kWT;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int64_t i = v * 8 + e;
+                        if (i < n && ((wd[e >> 1] >> (16 * (e & 1))) & 0xffffu) == 0u) {
+                            const uint32_t sl = atomicAdd(&sm.ncand, 1u);
+                            if (sl < (uint32_t)kCandCap) sm.ci[sl] = (uint32_t)i;
+                        }
                     }
                 }
             }
         }
         __syncthreads();
-        cnt = ncand < (uint32_t)kCandCap ? ncand : (uint32_t)kCandCap;
-        uint64_t kl = ~0ull, kh = 0;
+        cnt = sm.ncand < (uint32_t)kCandCap ? sm.ncand : (uint32_t)kCandCap;
         for (uint32_t j = (uint32_t)t; j < cnt; j += kWT) {
-            const uint64_t k = score_key(score[ci[j]]);
-            ck[j] = k;
+            const uint64_t k = score_key(score[sm.ci[j]]);
+            sm.ck[j] = k;
             kl = k < kl ? k : kl;
             kh = k > kh ? k : kh;
         }
-        kl = wave_min_u64(kl);
-        kh = wave_max_u64(kh);
-        if (lane == 0) {
-            wl[t / kWave] = kl;
-            wh[t / kWave] = kh;
-        }
         staged = true;
     } else {
-        uint64_t kl = ~0ull, kh = 0;
         for (int64_t i = t; i < n; i += kWT) {
             if (digit[i] == d0) {
                 const uint64_t k = score_key(score[i]);
@@ -325,32 +327,32 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
                 kh = k > kh ? k : kh;
             }
         }
-        kl = wave_min_u64(kl);
-        kh = wave_max_u64(kh);
-        if (lane == 0) {
-            wl[t / kWave] = kl;
-            wh[t / kWave] = kh;
-        }
+    }
+    kl = wave_min_u64(kl);
+    kh = wave_max_u64(kh);
+    if (lane == 0) {
+        sm.wl[t / kWave] = kl;
+        sm.wh[t / kWave] = kh;
     }
     __syncthreads();
     lo = ~0ull;
     hi = 0;
 #pragma unroll
     for (int w = 0; w < kWW; ++w) {
-        lo = wl[w] < lo ? wl[w] : lo;
-        hi = wh[w] > hi ? wh[w] : hi;
+        lo = sm.wl[w] < lo ? sm.wl[w] : lo;
+        hi = sm.wh[w] > hi ? sm.wh[w] : hi;
     }
     if (need == (int64_t)cnt) {
         reject_bin_and_above();
         return;
     }
 
-    // Finer levels until at most kPair candidates remain or they all share
+    // Finer levels until at most kRankMax candidates remain or they all share
     // one key (each level splits the key range by 2^kHBits, so six suffice).
     for (int level = 0; level < 8 && lo != hi; ++level) {
         if (!staged && cnt <= (uint32_t)kCandCap) {
             // One pass over the scores stages every key in [lo, hi].
-            if (t == 0) ncand = 0u;
+            if (t == 0) sm.ncand = 0u;
             __syncthreads();
             for (int64_t i = t; i < n; i += 4 * kWT) {
                 uint64_t k[4];
@@ -367,38 +369,38 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
                     if (m != 0ull) {
                         const int leader = __ffsll((long long)m) - 1;
                         uint32_t base = 0;
-                        if (lane == leader) base = atomicAdd(&ncand, (uint32_t)__popcll(m));
+                        if (lane == leader) base = atomicAdd(&sm.ncand, (uint32_t)__popcll(m));
                         base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
                         const uint32_t sl = base + (uint32_t)__popcll(m & lanes_below());
                         if (c && sl < (uint32_t)kCandCap) {
-                            ck[sl] = k[u];
-                            ci[sl] = (uint32_t)j;
+                            sm.ck[sl] = k[u];
+                            sm.ci[sl] = (uint32_t)j;
                         }
                     }
                 }
             }
             __syncthreads();
-            cnt = ncand < (uint32_t)kCandCap ? ncand : (uint32_t)kCandCap;
+            cnt = sm.ncand < (uint32_t)kCandCap ? sm.ncand : (uint32_t)kCandCap;
             staged = true;
         }
-        if (staged && cnt <= (uint32_t)kPair) break;
+        if (staged && cnt <= (uint32_t)kRankMax) break;
         // histogram of the candidates' next digit
         const int sh = range_shift(lo, hi);
-        for (int b = t; b < kHBins; b += kWT) h[b] = 0u;
+        for (int b = t; b < kHBins; b += kWT) sm.h[b] = 0u;
         __syncthreads();
         if (staged) {
             for (uint32_t j = (uint32_t)t; j < cnt; j += kWT) {
-                const uint64_t k = ck[j];
-                if (k >= lo && k <= hi) atomicAdd(&h[(k - lo) >> sh], 1u);
+                const uint64_t k = sm.ck[j];
+                if (k >= lo && k <= hi) atomicAdd(&sm.h[(k - lo) >> sh], 1u);
             }
         } else {
             for (int64_t i = t; i < n; i += kWT) {
                 const uint64_t k = score_key(score[i]);
-                if (k >= lo && k <= hi) atomicAdd(&h[(k - lo) >> sh], 1u);
+                if (k >= lo && k <= hi) atomicAdd(&sm.h[(k - lo) >> sh], 1u);
             }
         }
         __syncthreads();
-        pick(h[kHBins - 1 - 2 * t], h[kHBins - 2 - 2 * t], sh);
+        pick(sm.h[kHBins - 1 - 2 * t], sm.h[kHBins - 2 - 2 * t], sh);
         if (need == (int64_t)cnt) {
             reject_bin_and_above();
             return;
@@ -407,15 +409,15 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
             // keep the staged candidates that lie in the new range
             uint64_t kk[kCandCap / kWT];
             uint32_t ii[kCandCap / kWT];
-            const uint32_t c_old = ncand < (uint32_t)kCandCap ? ncand : (uint32_t)kCandCap;
+            const uint32_t c_old = sm.ncand < (uint32_t)kCandCap ? sm.ncand : (uint32_t)kCandCap;
 #pragma unroll
             for (int u = 0; u < kCandCap / kWT; ++u) {
                 const uint32_t j = (uint32_t)t + (uint32_t)u * kWT;
-                kk[u] = j < c_old ? ck[j] : 0ull;
-                ii[u] = j < c_old ? ci[j] : 0u;
+                kk[u] = j < c_old ? sm.ck[j] : 0ull;
+                ii[u] = j < c_old ? sm.ci[j] : 0u;
             }
             __syncthreads();
-            if (t == 0) ncand = 0u;
+            if (t == 0) sm.ncand = 0u;
             __syncthreads();
 #pragma unroll
             for (int u = 0; u < kCandCap / kWT; ++u) {
@@ -425,85 +427,93 @@ __global__ __launch_bounds__(kWT) void cut_select_kernel(const double *__restric
                 if (m != 0ull) {
                     const int leader = __ffsll((long long)m) - 1;
                     uint32_t base = 0;
-                    if (lane == leader) base = atomicAdd(&ncand, (uint32_t)__popcll(m));
+                    if (lane == leader) base = atomicAdd(&sm.ncand, (uint32_t)__popcll(m));
                     base = (uint32_t)__builtin_amdgcn_readlane((int)base, leader);
                     if (c) {
                         const uint32_t sl = base + (uint32_t)__popcll(m & lanes_below());
-                        ck[sl] = kk[u];
-                        ci[sl] = ii[u];
+                        sm.ck[sl] = kk[u];
+                        sm.ci[sl] = ii[u];
                     }
                 }
             }
             __syncthreads();
-            cnt = ncand;
+            cnt = sm.ncand;
         }
     }
 
-    if (lo == hi) {
-        // Every candidate has the key lo: the need-th lowest id among the
-        // trajectories with that key, by an ordered count over ids (thread t
-        // takes ids [t*per, (t+1)*per)).
-        const int64_t per = (n + kWT - 1) / kWT;
-        const int64_t j0 = (int64_t)t * per, j1 = (j0 + per < n) ? j0 + per : n;
-        uint32_t c = 0;
-        for (int64_t j = j0; j < j1; ++j) c += score_key(score[j]) == lo ? 1u : 0u;
-        uint32_t tot;
-        uint32_t before = block_excl_sum_u32<kWW>(c, tot, wsum);
-        if ((int64_t)before < need && need <= (int64_t)before + c) {
-            for (int64_t j = j0; j < j1; ++j) {
-                if (score_key(score[j]) == lo && (int64_t)(++before) == need) {
-                    s_id = j;
-                    break;
-                }
+    if (staged && cnt <= (uint32_t)kRankMax) {
+        // Rank by counting: candidate j gets threads 4j .. 4j + 3, each
+        // comparing it with every fourth candidate; the need-th largest
+        // (key desc, id asc) has rank need - 1.
+        const uint32_t j = (uint32_t)t >> 2, q = (uint32_t)t & 3u;
+        uint32_t r = 0;
+        uint64_t ka = 0;
+        uint32_t ia = 0;
+        if (j < cnt) {
+            ka = sm.ck[j];
+            ia = sm.ci[j];
+            for (uint32_t x = q; x < cnt; x += 4) {
+                const uint64_t kb = sm.ck[x];
+                const uint32_t ib = sm.ci[x];
+                r += (kb > ka || (kb == ka && ib < ia)) ? 1u : 0u;
             }
         }
-        __syncthreads();
-        if (t == 0) *out = CutRec{3, lo, s_id, 0};
+        r += (uint32_t)__shfl_xor((int)r, 1, kWave);
+        r += (uint32_t)__shfl_xor((int)r, 2, kWave);
+        if (j < cnt && q == 0u && (int64_t)r == need - 1) sm.cut = CutRec{3, ka, (int64_t)ia, 0};
         return;
     }
 
-    // At most kPair staged candidates in [lo, hi]: rank them pairwise.
-    if (t < kWave) {
-        const uint32_t c = cnt < (uint32_t)kPair ? cnt : (uint32_t)kPair;
-        if ((uint32_t)t < c) {
-            const uint64_t ka = ck[t];
-            const uint32_t ia = ci[t];
-            uint32_t r = 0;
-            for (uint32_t j = 0; j < c; ++j) {
-                const uint64_t kb = ck[j];
-                const uint32_t ib = ci[j];
-                r += (kb > ka || (kb == ka && ib < ia)) ? 1u : 0u;
-            }
-            if ((int64_t)r == need - 1) {
-                s_key = ka;
-                s_id = ia;
+    // Every candidate has the key lo (more of them than the ranking takes):
+    // the need-th lowest id among the trajectories with that key, by an
+    // ordered count over ids (thread t takes ids [t*per, (t+1)*per)).
+    const int64_t per = (n + kWT - 1) / kWT;
+    const int64_t j0 = (int64_t)t * per, j1 = (j0 + per < n) ? j0 + per : n;
+    uint32_t c = 0;
+    for (int64_t j = j0; j < j1; ++j) c += score_key(score[j]) == lo ? 1u : 0u;
+    uint32_t tot;
+    uint32_t before = block_excl_sum_u32<kWW>(c, tot, sm.wsum);
+    if ((int64_t)before < need && need <= (int64_t)before + c) {
+        for (int64_t j = j0; j < j1; ++j) {
+            if (score_key(score[j]) == lo && (int64_t)(++before) == need) {
+                sm.cut = CutRec{3, lo, j, 0};
+                break;
             }
         }
     }
-    __syncthreads();
-    if (t == 0) *out = CutRec{3, s_key, s_id, 0};
 }
 
-// One thread per trajectory: the keep flag from the cut; then the partials
-// of each block of kWideBlock trajectories (one wave): kept count, kept
-// tokens (spans clamped to [0, NT]) and pieces (wide_block_pieces; zero
-// without offsets).
-__global__ __launch_bounds__(256) void classify_kernel(const double *__restrict__ score,
+// One 1024-thread workgroup per 1024 trajectories: the cut (find_cut, the
+// same in every workgroup), then per trajectory the keep flag, and per block
+// of kWideBlock trajectories (one wave) the kept count, kept tokens (spans
+// clamped to [0, NT]) and pieces (wide_block_pieces; zero without offsets).
+// Workgroup 0 also stores the cut.
+__global__ __launch_bounds__(kWT) void classify_kernel(const double *__restrict__ score,
                                                        const int64_t *__restrict__ off, int64_t n, int64_t NT,
-                                                       const CutRec *__restrict__ cut_p, uint8_t *__restrict__ keep,
-                                                       PieceParts parts) {
+                                                       int64_t budget, const uint32_t *__restrict__ hist,
+                                                       const uint16_t *__restrict__ digit,
+                                                       const uint64_t *__restrict__ range, CutRec *__restrict__ cut,
+                                                       uint8_t *__restrict__ keep, PieceParts parts) {
     static_assert(kWideBlock == kWave, "a wide block is one wave");
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const CutRec c = *cut_p;
-    bool kept = false;
-    int64_t len = 0;
+    __shared__ CutSmem sm;
+    const int64_t i = (int64_t)blockIdx.x * kWT + threadIdx.x;
+    // This thread's trajectory first: its loads do not wait for the cut.
+    double sc = 0.0;
+    int64_t lo = 0, hi = 0;
     if (i < n) {
-        const double sc = score[i];
-        int64_t lo = 0, hi = 0;
+        sc = score[i];
         if (off) {
             lo = clamp64(off[i], 0, NT);
             hi = clamp64(off[i + 1], 0, NT);
         }
+    }
+    find_cut(score, n, budget, hist, digit, range, sm);
+    __syncthreads();
+    const CutRec c = sm.cut;
+    if (blockIdx.x == 0 && threadIdx.x == 0) *cut = c;
+    bool kept = false;
+    int64_t len = 0;
+    if (i < n) {
         kept = !cut_rejects(c, score_key(sc), i);
         keep[i] = kept ? 1 : 0;
         len = kept && hi > lo ? hi - lo : 0;
@@ -579,18 +589,16 @@ hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const
     if (n == 0) return hipSuccess;
     const int64_t g = wide_hist_wgs(n);
     const int64_t per = (n + g - 1) / g;
-    hipError_t e = launch(kPhaseSelect, cut_hist_kernel, dim3((unsigned)g), dim3(kWT), stream, score, n, w.mmin,
-                          w.mmax, w.n_mm, per, w.hist, w.digit, w.range);
-    if (e != hipSuccess) return e;
-    return launch(kPhaseSelect, cut_select_kernel, dim3(1), dim3(kWT), stream, score, n, budget, w.hist, w.digit,
-                  w.range, w.cut);
+    return launch(kPhaseSelect, cut_hist_kernel, dim3((unsigned)g), dim3(kWT), stream, score, n, w.mmin,
+                  w.mmax, w.n_mm, per, w.hist, w.digit, w.range);
 }
 
 hipError_t launch_classify(const double *score, const int64_t *offsets, int64_t n, int64_t n_tokens,
-                           const WideWs &w, uint8_t *keep, const PieceParts &parts, hipStream_t stream) {
+                           int64_t budget, const WideWs &w, uint8_t *keep, const PieceParts &parts,
+                           hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    return launch(kPhaseSelect, classify_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), stream, score,
-                  offsets, n, n_tokens, w.cut, keep, parts);
+    return launch(kPhaseSelect, classify_kernel, dim3((unsigned)((n + kWT - 1) / kWT)), dim3(kWT), stream,
+                  score, offsets, n, n_tokens, budget, w.hist, w.digit, w.range, w.cut, keep, parts);
 }
 
 hipError_t launch_emit_rejects_wide(const uint8_t *keep, int64_t n, const int32_t *kept_cnt, int64_t budget,
