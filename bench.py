@@ -11,8 +11,10 @@ between one event pair over rotating copies of the pool, so that every step
 starts with its copy out of the L2 and the 256 MB MALL.
 
 The same measurement is repeated for the other pools (tiny, single-turn math,
-long reasoning, multi-turn tool use, and the stress pool with three payload
-columns) under "configs", each with the oracle timed on the same pool; the
+long reasoning, multi-turn tool use, the stress pool with three payload
+columns, and the wide pool: 65536 trajectories of log-normal lengths around
+700 tokens, 52.1M tokens, target 21845) under "configs", each with the oracle
+timed on the same pool; the
 256-step sweep of the exact top-b step (V + 1 and 5% of the slots refreshed
 per step, beta 0 and 0.9 with the smoothed rate carried) is under
 "topb_sweep".
@@ -47,7 +49,7 @@ def parse():
     ap.add_argument("--mode", default="effective", choices=["effective", "raw", "gen"])
     ap.add_argument("--cols", type=int, default=1, choices=[1, 3],
                     help="payload columns: 1 = tags; 3 = tags + token ids + fp32 log-probs")
-    ap.add_argument("--configs", default="tiny,math,long,multiturn,stress3",
+    ap.add_argument("--configs", default="tiny,math,long,multiturn,stress3,wide",
                     help="pools measured besides the headline ('' = none); stress3 = stress with 3 columns")
     ap.add_argument("--topb-steps", type=int, default=256,
                     help="steps of the exact top-b sweep (0 = skip)")
@@ -62,9 +64,12 @@ def parse():
     return ap.parse_args()
 
 
-# (timer phase, kernel) of the fused step's launches for pools of up to 8192
-# trajectories
+# (timer phase, kernel) of the fused step's launches: pools of up to 8192
+# trajectories (rank path), and larger ones (level-0 histogram of the cut
+# search, cut-and-classify, compaction with blocks of 64 trajectories)
 PHASES = ((0, "score_reduce"), (1, "score_finalize"), (2, "rank"), (3, "compact_piece"))
+PHASES_WIDE = ((0, "score_reduce"), (1, "score_finalize"), (2, "cut_hist"), (6, "classify"),
+               (3, "compact_piece"))
 
 
 def cpu_model():
@@ -93,23 +98,36 @@ def kernel_bytes(pool, n_keep_tok, col_bytes, W, use_prefix, cus):
                    (piece sum and count written), 16 B per chunk (carry);
     score_finalize offsets (2 x 8 B), completion 4 B, prefix score 8 B and
                    the window when used, the pieces (16 B per trajectory and
-                   per chunk) read; score 8 B, S and T 16 B written;
+                   per chunk) read; score 8 B, S and T 16 B written (pools
+                   above 8192 trajectories: plus the group key extremes,
+                   16 B per 128 trajectories);
     rank           score 8 B and span offsets 16 B read, keep flag 1 B and the
                    block partials (16 B per 16 trajectories) written;
+    cut_hist       score 8 B read and level-0 digit 2 B written per
+                   trajectory, the group extremes read, the 2048-bin
+                   histogram (8 KiB) added;
+    classify       score 8 B, offsets 16 B and digit 2 B read, keep flag 1 B
+                   written per trajectory, the histogram read, the block
+                   partials (16 B per 64 trajectories) written;
     compact_piece  every kept element of each column read and written, keep
                    flags and offsets (17 B per trajectory), the block
                    partials, packed offsets (8 B) and kept ids (4 B) per kept
                    trajectory and rejected ids (4 B per rejection) written."""
     n, N = pool.n, pool.n_tokens
     chunks = reduce_chunks(N, cus)
-    blocks = -(-n // 16)
+    wide = n > 8192
+    blk = 64 if wide else 16
+    blocks = -(-n // blk)
+    groups = -(-n // 128)
     budget = max(0, pool.occupancy - pool.capacity)
     kept = n - min(budget, n)
     pre = (8 * n + 8 * W) if use_prefix else 0
     return {
         "score_reduce": 4 * N + 8 * (n + 1) + 16 * n + 16 * chunks,
-        "score_finalize": 16 * n + 4 * n + pre + 16 * n + 16 * chunks + 8 * n + 16 * n,
+        "score_finalize": 16 * n + 4 * n + pre + 16 * n + 16 * chunks + 8 * n + 16 * n + (16 * groups if wide else 0),
         "rank": 8 * n + 16 * n + n + 16 * blocks,
+        "cut_hist": 8 * n + 2 * n + 16 * groups + 8192,
+        "classify": 8 * n + 16 * n + 2 * n + n + 8192 + 16 * blocks,
         "compact_piece": sum(2 * e * n_keep_tok for e in col_bytes) + 17 * n + 16 * blocks
                          + 12 * kept + 8 + 4 * budget,
     }
@@ -235,8 +253,8 @@ def measure_pool(pace, pool, host_cols, mode, K, dev, stream, cus, config_name):
     ms = ev[0].elapsed_time(ev[1]) / K
     assert int(rot.nkt.item()) == n_keep_tok
     # each kernel timed by its own events, same rotation
-    big = pool.n <= 8192
-    kev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in PHASES]
+    phases = PHASES if pool.n <= 8192 else PHASES_WIDE
+    kev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in phases]
            for _ in range(K)]
     for pairs in kev:
         for a, b in pairs:
@@ -244,15 +262,15 @@ def measure_pool(pace, pool, host_cols, mode, K, dev, stream, cus, config_name):
             b.record(stream)
     torch.cuda.synchronize()
     for k in range(K):
-        for m, (ph, _) in enumerate(PHASES):
+        for m, (ph, _) in enumerate(phases):
             pace.pace_time_next_kernel(ph, *kev[k][m])
         rot.step(k)
     torch.cuda.synchronize()
     kus = {name: float(np.mean([kev[k][m][0].elapsed_time(kev[k][m][1]) * 1e3 for k in range(K)]))
-           for m, (_, name) in enumerate(PHASES)}
+           for m, (_, name) in enumerate(phases)}
     B = alg_bytes(pool, n_keep_tok, rot.col_bytes, rot.W, rot.prefix is not None)
     kb = kernel_bytes(pool, n_keep_tok, rot.col_bytes, rot.W, rot.prefix is not None, cus)
-    dom = max(kus, key=kus.get) if big else "score_reduce"
+    dom = max(kus, key=kus.get)
     t_dom = kus[dom] * 1e-6
     res = {
         "n_traj": pool.n, "n_tokens": pool.n_tokens, "budget": budget, "kept_tokens": n_keep_tok,

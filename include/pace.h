@@ -404,11 +404,14 @@ int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t 
  * thread. Calls on other threads never see it.
  * phase: PACE_PHASE_REDUCE (token reduction of pace_score), PACE_PHASE_FINALIZE
  *   (score finalisation), PACE_PHASE_SELECT (the rank kernel, the
- *   single-workgroup select of large pools, or the streaming draw),
+ *   single-workgroup select of the largest pools, or the streaming draw),
  *   PACE_PHASE_COMPACT (the compaction copy kernel), PACE_PHASE_PREFIX (the
  *   Prefix Forgetting Score kernel), PACE_PHASE_AUX (the single kernel of
  *   pace_group_score, pace_group_expand, pace_stale_k or pace_diagnostics,
- *   or the window-cutoff kernel of the streaming rule).
+ *   or the window-cutoff kernel of the streaming rule), PACE_PHASE_CLASSIFY
+ *   (pools above 8192 trajectories: the kernel that finds the rejection cut
+ *   and writes the keep flags; PACE_PHASE_SELECT then times the level-0
+ *   histogram of that cut search).
  * start_event, stop_event: hipEvent_t handles created by the caller with
  *   timing enabled; both NULL disarms the phase. The caller keeps ownership.
  * Returns PACE_ERR_INVALID_ARG for an unknown phase or one NULL event. */
@@ -418,7 +421,8 @@ int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t 
 #define PACE_PHASE_COMPACT 3
 #define PACE_PHASE_PREFIX 4
 #define PACE_PHASE_AUX 5
-#define PACE_PHASE_COUNT 6
+#define PACE_PHASE_CLASSIFY 6
+#define PACE_PHASE_COUNT 7
 int pace_time_next_kernel(int phase, void *start_event, void *stop_event);
 
 /* Static description of an error code. */

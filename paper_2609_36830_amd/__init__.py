@@ -32,7 +32,8 @@ __all__ = [
 
 WS_SCORE, WS_SELECT, WS_COMPACT, WS_FILTER_STEP = 0, 1, 2, 3
 BAD_OFFSETS, BAD_COMPLETION, BAD_TAG, BAD_WINDOW, BAD_GROUPS = 0x1, 0x2, 0x4, 0x8, 0x10
-PHASE_REDUCE, PHASE_FINALIZE, PHASE_SELECT, PHASE_COMPACT, PHASE_PREFIX, PHASE_AUX = 0, 1, 2, 3, 4, 5
+PHASE_REDUCE, PHASE_FINALIZE, PHASE_SELECT, PHASE_COMPACT, PHASE_PREFIX, PHASE_AUX, PHASE_CLASSIFY = \
+    0, 1, 2, 3, 4, 5, 6
 
 
 class PaceError(RuntimeError):

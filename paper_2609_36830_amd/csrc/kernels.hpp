@@ -20,7 +20,7 @@ int64_t resident_waves();
 // launched with hipExtLaunchKernel and the two events, which then bracket
 // the kernel's own execution; the timer is consumed by that launch.
 enum TimedPhase : int { kPhaseReduce = 0, kPhaseFinalize = 1, kPhaseSelect = 2, kPhaseCompact = 3,
-                        kPhasePrefix = 4, kPhaseAux = 5, kPhaseCount = 6 };
+                        kPhasePrefix = 4, kPhaseAux = 5, kPhaseClassify = 6, kPhaseCount = 7 };
 bool take_phase_timer(int phase, hipEvent_t *start, hipEvent_t *stop);
 
 template <typename... P, typename... A>

@@ -597,7 +597,7 @@ hipError_t launch_classify(const double *score, const int64_t *offsets, int64_t 
                            int64_t budget, const WideWs &w, uint8_t *keep, const PieceParts &parts,
                            hipStream_t stream) {
     if (n == 0) return hipSuccess;
-    return launch(kPhaseSelect, classify_kernel, dim3((unsigned)((n + kWT - 1) / kWT)), dim3(kWT), stream,
+    return launch(kPhaseClassify, classify_kernel, dim3((unsigned)((n + kWT - 1) / kWT)), dim3(kWT), stream,
                   score, offsets, n, n_tokens, budget, w.hist, w.digit, w.range, w.cut, keep, parts);
 }
 

@@ -221,12 +221,12 @@ def test_select_and_compact_host_argument_errors(L):
 
 def test_time_next_kernel_arguments(L):
     assert L.pace_time_next_kernel(-1, None, None) == -1
-    assert L.pace_time_next_kernel(6, None, None) == -1
+    assert L.pace_time_next_kernel(7, None, None) == -1
     assert L.pace_time_next_kernel(0, FAKE, None) == -1
     assert L.pace_time_next_kernel(0, None, FAKE) == -1
     # arm then disarm: nothing is launched, so the fake handles are never used
     assert L.pace_time_next_kernel(3, FAKE, FAKE) == 0
-    for phase in range(6):
+    for phase in range(7):
         assert L.pace_time_next_kernel(phase, None, None) == 0
 
 

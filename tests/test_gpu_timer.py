@@ -77,3 +77,21 @@ def test_timer_reaches_the_next_device_call(pace):
     pace.pace_compact(off, keep, [tags])
     torch.cuda.synchronize()
     assert a.elapsed_time(b) == t
+
+
+def test_wide_pool_phases_are_timed(pace):
+    """Above 8192 trajectories the filter step times the cut histogram as the
+    select phase and the cut-and-classify kernel as its own phase."""
+    import poolgen
+    from tests.test_gpu_parity import gpu_step
+    pool = poolgen.make_pool("wide", n=20000)
+    say("timer: wide pool n=%d, select, classify and compact phases armed" % pool.n)
+    ev = {ph: _events() for ph in (pace.PHASE_SELECT, pace.PHASE_CLASSIFY, pace.PHASE_COMPACT)}
+    before = {ph: a.elapsed_time(b) for ph, (a, b) in ev.items()}
+    for ph, (a, b) in ev.items():
+        pace.pace_time_next_kernel(ph, a, b)
+    gpu_step(pace, pool, fused=True)
+    torch.cuda.synchronize()
+    for ph, (a, b) in ev.items():
+        t = a.elapsed_time(b)
+        assert t != before[ph] and t > 0, ph
