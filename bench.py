@@ -86,9 +86,9 @@ def cpu_model():
 
 def reduce_chunks(n_tokens, cus):
     """Token chunks of score_reduce: one per resident wave (CUs x 16),
-    2048-token aligned."""
+    256-token aligned, at least 2048 tokens."""
     waves = cus * 16
-    chunk = max(2048, -(-(-(-n_tokens // waves)) // 2048) * 2048)
+    chunk = max(2048, -(-(-(-n_tokens // waves)) // 256) * 256)
     return -(-n_tokens // chunk)
 
 

@@ -46,20 +46,25 @@ hipError_t launch(int phase, void (*kernel)(P...), dim3 grid, dim3 block, hipStr
 // measured much slower).
 constexpr int kReduceWavesPerCU = 16;
 // One wave reduces one chunk of consecutive tokens; the chunk length is a
-// multiple of kScoreChunkAlign chosen so that the chunks fill the device once.
-constexpr int64_t kScoreChunkAlign = 2048;
+// multiple of kScoreChunkAlign (one 256-token window, 1 KiB of tags) chosen so
+// that the chunks fill the device once, and at least kScoreChunkMin (which
+// bounds the number of chunks, and so the carry arrays, by n_tokens / 2048).
+// A coarser alignment would leave waves idle: 52.1M tokens over 4096 waves is
+// 12,721 per wave, which 2048-token alignment rounds to 14,336 (3636 chunks).
+constexpr int64_t kScoreChunkAlign = 256;
+constexpr int64_t kScoreChunkMin = 2048;
 // Largest prefix window staged in LDS by the finalize kernel.
 constexpr int64_t kWindowLdsMax = 4096;
 
 inline int64_t score_chunk_len(int64_t n_tokens, int64_t waves) {
     int64_t per = (n_tokens + waves - 1) / (waves > 0 ? waves : 1);
     per = (per + kScoreChunkAlign - 1) / kScoreChunkAlign * kScoreChunkAlign;
-    return per > kScoreChunkAlign ? per : kScoreChunkAlign;
+    return per > kScoreChunkMin ? per : kScoreChunkMin;
 }
 // Upper bound on the chunk count for any device (the chunk is never shorter
-// than kScoreChunkAlign).
+// than kScoreChunkMin).
 inline int64_t score_max_chunks(int64_t n_tokens) {
-    return (n_tokens + kScoreChunkAlign - 1) / kScoreChunkAlign;
+    return (n_tokens + kScoreChunkMin - 1) / kScoreChunkMin;
 }
 
 struct ScoreWorkspace {

@@ -3,8 +3,8 @@
 // Step 1 (score_reduce): every per-token version tag is read exactly once.
 // The token array is cut into equal chunks of consecutive tokens, one per
 // wave64, sized so that every resident wave gets exactly one (a multiple of
-// 2048 tokens); a chunk is read as 16-byte vectors, 8 per lane in flight, the
-// first batch issued before the trajectory search. (Plain loads on purpose:
+// 256 tokens, at least 2048); a chunk is read as 16-byte vectors, 8 per lane
+// in flight, the first batch issued before the trajectory search. (Plain loads on purpose:
 // they leave the tags in the last-level cache, where the compaction re-reads
 // the kept spans.) Let G(p) be the sum of (tag + 1) over the generated tokens
 // of [chunk start, p) (masked tags, -1, add 0) and their count. The wave holds
@@ -41,21 +41,28 @@ namespace {
 constexpr int kVec = 4;                       // tags per lane per window
 constexpr int kWin = kWave * kVec;            // 256 tokens per wave window
 constexpr int kUnroll = 8;                    // windows per super-window
-constexpr int kSub = 4;                       // windows per fast-path / walk block
+constexpr int kSub = 4;                       // windows per block of the fast path
 constexpr int kWavesPerBlock = 4;
-static_assert(kScoreChunkAlign % (kWin * kUnroll) == 0, "chunk must be a multiple of the super-window");
+static_assert(kScoreChunkAlign % kWin == 0, "a chunk is whole windows");
 
-// Position-ordered prefixes of one block (kSub windows, kBlk tokens) for the
-// trajectory boundaries inside it, per wave: window-local exclusive prefix
-// sums of (tag + 1) (32-bit when every tag + 1 < 2^24: a window sums below
-// 2^32) and of the generated-token count (at most 255 before the last
-// position of a window, so one byte).
-constexpr int kBlk = kSub * kWin;
-template <bool kNarrow>
-struct BlockPrefix {
-    using S = typename std::conditional<kNarrow, uint32_t, uint64_t>::type;
-    S s[kWavesPerBlock][kBlk];
-    uint8_t c[kWavesPerBlock][kBlk];
+// Arithmetic of the reduction, chosen from V (tags are at most V):
+//   kPacked  every tag + 1 < 2^15: an element is q = (tag + 1) * 2^9 +
+//            [tag != -1], so that a window's 256 elements sum below 2^32 with
+//            the count in the low 9 bits; one 32-bit scan gives both prefixes,
+//            and a lane's running sums are kept as sum * 2^24 + count in 64
+//            bits (one wave reduction for both);
+//   kNarrow  every tag + 1 < 2^24: 32-bit window sums, counts separate;
+//   kWide    64-bit sums.
+enum ReduceMode : int { kPacked = 0, kNarrow = 1, kWideTags = 2 };
+
+// Window-local exclusive prefixes of one window per wave, for the trajectory
+// boundaries inside it: sums (with the packed count), and for the other modes
+// the counts (at most 255 before a window's last position, so one byte).
+template <int kMode>
+struct WinPrefix {
+    using S = typename std::conditional<kMode == kWideTags, uint64_t, uint32_t>::type;
+    S s[kWavesPerBlock][kWin];
+    uint8_t c[kWavesPerBlock][kMode == kPacked ? 4 : kWin];
 };
 
 __device__ __forceinline__ uint32_t wave_incl_add(uint32_t v) { return wave_incl_scan_u32(v); }
@@ -85,6 +92,11 @@ __device__ __forceinline__ void add_all_wide(const int4 &v, uint64_t &s, uint32_
     c += (u0 != 0u) + (u1 != 0u) + (u2 != 0u) + (u3 != 0u);
 }
 
+// Packed element: (x + 1) * 2^9 + 1 for a tag x >= 0, 0 for x = -1.
+__device__ __forceinline__ uint32_t packed(int x) {
+    return ((uint32_t)x << 9) + 513u + (uint32_t)(x >> 31);
+}
+
 template <bool kVecLoad, int U>
 __device__ __forceinline__ void load_super(const int32_t *__restrict__ tags, int64_t pos, int64_t ce,
                                            int lane, int4 (&v)[U]) {
@@ -103,16 +115,14 @@ __device__ __forceinline__ void load_super(const int32_t *__restrict__ tags, int
     }
 }
 
-// kNarrow: every tag + 1 < 2^24, so a lane's 16 tags of one block sum below
-// 2^28 in 32 bits before widening, and a window's 256 below 2^32.
-template <bool kNarrow, bool kVecLoad, int U = kUnroll>
+template <int kMode, bool kVecLoad, int U = kUnroll>
 __global__ __launch_bounds__(256) void score_reduce_kernel(
     const int32_t *__restrict__ tags, const int64_t *__restrict__ off, int64_t n, int64_t NT,
     int64_t chunk_len, int64_t n_chunks, uint64_t *__restrict__ part_sum,
     int64_t *__restrict__ part_cnt, uint64_t *__restrict__ carry_sum,
     int64_t *__restrict__ carry_cnt) {
-    using PS = typename BlockPrefix<kNarrow>::S;
-    __shared__ BlockPrefix<kNarrow> lds;
+    using PS = typename WinPrefix<kMode>::S;
+    __shared__ WinPrefix<kMode> lds;
     const int lane = lane_id();
     const int wv = threadIdx.x / kWave;
     const int64_t chunk = (int64_t)blockIdx.x * kWavesPerBlock + wv;
@@ -171,19 +181,41 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
     // in this chunk is the difference of two neighbouring lanes.
     uint64_t Gs = 0;
     int64_t Gc = 0;
-    uint64_t Ws = 0;             // G at the current block's start, less what acc_* still hold
+    uint64_t Ws = 0;             // G at the current window's start, less what acc_* still hold
     int64_t Wc = 0;
-    uint64_t acc_s = 0;          // per-lane sums of blocks without a boundary
+    uint64_t acc_s = 0;          // per-lane sums of windows without a boundary (kPacked: sum * 2^24 + count)
     uint32_t acc_c = 0;
     bool dirty = false;
     auto sync = [&]() {
         if (dirty) {
-            Ws += wave_sum_u64(acc_s);
-            Wc += (int64_t)wave_sum_u64((uint64_t)acc_c);
+            if constexpr (kMode == kPacked) {
+                const uint64_t t = wave_sum_u64(acc_s);
+                Ws += t >> 24;
+                Wc += (int64_t)(t & 0xffffffull);
+            } else {
+                Ws += wave_sum_u64(acc_s);
+                Wc += (int64_t)wave_sum_u64((uint64_t)acc_c);
+            }
             acc_s = 0;
             acc_c = 0;
             dirty = false;
         }
+    };
+    // Adds nv vectors (a window or a block without boundaries) per lane.
+    auto add_vecs = [&](const int4 *vb, int nv) {
+        if constexpr (kMode == kWideTags) {
+            for (int k = 0; k < nv; ++k) add_all_wide(vb[k], acc_s, acc_c);
+        } else {
+            uint32_t s32 = 0, c32 = 0;             // below 2^28 for up to 16 tags per lane
+            for (int k = 0; k < nv; ++k) add_all(vb[k], s32, c32);
+            if constexpr (kMode == kPacked) {
+                acc_s += ((uint64_t)s32 << 24) + c32;
+            } else {
+                acc_s += s32;
+                acc_c += c32;
+            }
+        }
+        dirty = true;
     };
     // Smallest boundary still ahead (wave-uniform).
     int64_t next_b;
@@ -217,7 +249,7 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
         const bool has = lane < kWave - 1 && j < n && B1 > B && B < ce && B1 > cs;
         at = !has ? -2 : (B >= cs ? j : -1);
     };
-    // Every boundary of the window lies before the current block's end:
+    // Every boundary of the window lies before the current window's end:
     // keep its pieces and move to the next window.
     auto next_window = [&]() {
         int64_t at, pc;
@@ -237,55 +269,60 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
         Gc = lane == 0 ? g_c : 0;
     };
 
-    // A block holding boundaries: window-local prefixes into LDS, then every
-    // lane whose boundary falls in the block reads its G.
-    auto slow_block = [&](const int4 *v, int64_t bpos, int64_t bend) {
+    // A window [w, w_end) holding boundaries: its exclusive prefixes into
+    // LDS, then every lane whose boundary falls in the window reads its G.
+    auto event_window = [&](const int4 &v, int64_t w, int64_t w_end) {
         sync();
-        uint64_t wpre_s[kSub];
-        int64_t wpre_c[kSub];
-        uint64_t run_s = 0;
-        int64_t run_c = 0;
-#pragma unroll
-        for (int k = 0; k < kSub; ++k) {
-            wpre_s[k] = run_s;
-            wpre_c[k] = run_c;
-            const uint32_t u0 = (uint32_t)v[k].x + 1u, u1 = (uint32_t)v[k].y + 1u;
-            const uint32_t u2 = (uint32_t)v[k].z + 1u, u3 = (uint32_t)v[k].w + 1u;
+        uint64_t tot_s;
+        int64_t tot_c;
+        PS *ds = pre_s + lane * kVec;
+        if constexpr (kMode == kPacked) {
+            const uint32_t q0 = packed(v.x), q1 = packed(v.y), q2 = packed(v.z), q3 = packed(v.w);
+            const uint32_t p1 = q0, p2 = p1 + q1, p3 = p2 + q2, p4 = p3 + q3;
+            const uint32_t is = wave_incl_scan_u32(p4);
+            const uint32_t es = is - p4;
+            ds[0] = es;
+            ds[1] = es + p1;
+            ds[2] = es + p2;
+            ds[3] = es + p3;
+            const uint32_t t = (uint32_t)__builtin_amdgcn_readlane((int)is, kWave - 1);
+            tot_s = t >> 9;
+            tot_c = t & 511u;
+        } else {
+            const uint32_t u0 = (uint32_t)v.x + 1u, u1 = (uint32_t)v.y + 1u;
+            const uint32_t u2 = (uint32_t)v.z + 1u, u3 = (uint32_t)v.w + 1u;
             const PS p1 = (PS)u0, p2 = p1 + (PS)u1, p3 = p2 + (PS)u2, p4 = p3 + (PS)u3;
             const uint32_t c1 = (u0 != 0u), c2 = c1 + (u1 != 0u), c3 = c2 + (u2 != 0u), c4 = c3 + (u3 != 0u);
             const PS is = wave_incl_add(p4);
             const uint32_t ic = wave_incl_scan_u32(c4);
             const PS es = is - p4;
             const uint32_t ec = ic - c4;
-            PS *ds = pre_s + k * kWin + lane * kVec;
             ds[0] = es;
             ds[1] = es + p1;
             ds[2] = es + p2;
             ds[3] = es + p3;
-            *reinterpret_cast<uint32_t *>(pre_c + k * kWin + lane * kVec) =
+            *reinterpret_cast<uint32_t *>(pre_c + lane * kVec) =
                 ec | ((ec + c1) << 8) | ((ec + c2) << 16) | ((ec + c3) << 24);
-            if constexpr (kNarrow) {
-                run_s += (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)is, kWave - 1);
+            if constexpr (kMode == kNarrow) {
+                tot_s = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)is, kWave - 1);
             } else {
-                run_s += (uint64_t)readlane_i64((int64_t)is, kWave - 1);
+                tot_s = (uint64_t)readlane_i64((int64_t)is, kWave - 1);
             }
-            run_c += (int64_t)(uint32_t)__builtin_amdgcn_readlane((int)ic, kWave - 1);
+            tot_c = (int64_t)(uint32_t)__builtin_amdgcn_readlane((int)ic, kWave - 1);
         }
         while (true) {
-            if (B >= bpos && B < bend) {
-                const int q = (int)(B - bpos);
-                const int k = q / kWin;
-                uint64_t ws = wpre_s[0];
-                int64_t wc = wpre_c[0];
-#pragma unroll
-                for (int kk = 1; kk < kSub; ++kk) {
-                    ws = k == kk ? wpre_s[kk] : ws;
-                    wc = k == kk ? wpre_c[kk] : wc;
+            if (B >= w && B < w_end) {
+                const int q = (int)(B - w);
+                if constexpr (kMode == kPacked) {
+                    const uint32_t p = (uint32_t)pre_s[q];
+                    Gs = Ws + (p >> 9);
+                    Gc = Wc + (int64_t)(p & 511u);
+                } else {
+                    Gs = Ws + (uint64_t)pre_s[q];
+                    Gc = Wc + (int64_t)pre_c[q];
                 }
-                Gs = Ws + ws + (uint64_t)pre_s[q];
-                Gc = Wc + wc + (int64_t)pre_c[q];
             }
-            const uint64_t m = ballot(B >= bend);
+            const uint64_t m = ballot(B >= w_end);
             if (m) {
                 next_b = readlane_i64(B, __ffsll((long long)m) - 1);
                 break;
@@ -296,38 +333,57 @@ __global__ __launch_bounds__(256) void score_reduce_kernel(
             }
             next_window();
         }
-        Ws += run_s;
-        Wc += run_c;
+        Ws += tot_s;
+        Wc += tot_c;
     };
 
-    // Adds the kSub vectors at vb (a block without boundaries).
-    auto add_block = [&](const int4 *vb) {
-        if (kNarrow) {
-            uint32_t s32 = 0, c32 = 0;
-#pragma unroll
-            for (int k = 0; k < kSub; ++k) add_all(vb[k], s32, c32);
-            acc_s += s32;
-            acc_c += c32;
-        } else {
-#pragma unroll
-            for (int k = 0; k < kSub; ++k) add_all_wide(vb[k], acc_s, acc_c);
+    // Adds block h of the super-window in v (kSub windows from bpos): a block
+    // without boundaries is added per lane; in a block with boundaries each
+    // window without one is added per lane, the others go to event_window.
+    auto process_block = [&](int4 (&v)[U], int64_t bpos, int h) {
+        if (bpos >= ce) return;
+        const int64_t bend = (bpos + kSub * kWin < ce) ? bpos + kSub * kWin : ce;
+        if (next_b >= bend) {
+            add_vecs(v + h * kSub, kSub);
+            return;
         }
-        dirty = true;
+#pragma unroll
+        for (int k = 0; k < kSub; ++k) {
+            const int64_t w = bpos + (int64_t)k * kWin;
+            if (w >= ce) break;
+            const int64_t w_end = (w + kWin < ce) ? w + kWin : ce;
+            if (next_b >= w_end) add_vecs(v + h * kSub + k, 1);
+            else event_window(v[h * kSub + k], w, w_end);
+        }
     };
 
+    auto load_half = [&](int64_t p, int half) {
+#pragma unroll
+        for (int k = 0; k < kSub; ++k) {
+            const int64_t q = p + (int64_t)k * kWin + (int64_t)lane * kVec;
+            int4 &x = va[half * kSub + k];
+            if (kVecLoad && q + kVec <= ce) {
+                x = *reinterpret_cast<const int4 *>(tags + q);
+            } else {
+                x = make_int4(-1, -1, -1, -1);
+                if (q < ce) x.x = tags[q];
+                if (q + 1 < ce) x.y = tags[q + 1];
+                if (q + 2 < ce) x.z = tags[q + 2];
+                if (q + 3 < ce) x.w = tags[q + 3];
+            }
+        }
+    };
+    // Each half of the next super-window is loaded as soon as the same half
+    // of this one has been added, so loads stay queued while the other half
+    // is processed.
     for (int64_t pos = cs; pos < ce; pos += kSuper) {
-        if (pos != cs) {
+        process_block(va, pos, 0);
+        if (pos + kSuper < ce) {
             if (want_next()) load_next();
-            load_super<kVecLoad>(tags, pos, ce, lane, va);
+            load_half(pos + kSuper, 0);
         }
-#pragma unroll
-        for (int h = 0; h < U / kSub; ++h) {
-            const int64_t bpos = pos + (int64_t)h * kBlk;
-            if (bpos >= ce) break;
-            const int64_t bend = (bpos + kBlk < ce) ? bpos + kBlk : ce;
-            if (next_b >= bend) add_block(va + h * kSub);
-            else slow_block(va + h * kSub, bpos, bend);
-        }
+        process_block(va, pos + kSub * kWin, 1);
+        if (pos + kSuper + kSub * kWin < ce) load_half(pos + kSuper + kSub * kWin, 1);
     }
     sync();
     if (B >= ce) {
@@ -356,7 +412,7 @@ __global__ __launch_bounds__(kFinT) void score_finalize_kernel(
     double *__restrict__ score, int64_t *__restrict__ gen_sum, int64_t *__restrict__ gen_count,
     uint64_t *__restrict__ mmin, uint64_t *__restrict__ mmax, uint32_t *__restrict__ hist0) {
     __shared__ double win_lds[kWinLds ? kWindowLdsMax : 1];
-    const bool narrow = (NT >> 11) < ((int64_t)1 << 32);   // token positions below 2^43
+    const bool narrow = (NT >> 8) < ((int64_t)1 << 32);    // token positions below 2^40
     // The trajectory's own loads go first (they do not wait for the window),
     // then the window is staged; every thread reaches the barrier.
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -439,15 +495,18 @@ hipError_t launch_score_reduce(const int32_t *tags, const int64_t *offsets, int6
     const int64_t ch = n_tokens > 0 ? (n_tokens + chunk_len - 1) / chunk_len : 0;
     if (n == 0 || ch == 0) return hipSuccess;
     const unsigned grid = (unsigned)((ch + kWavesPerBlock - 1) / kWavesPerBlock);
-    const bool narrow = (int64_t)V < (1 << 24) - 1;
-#define PACE_REDUCE(NARROW, VEC)                                                            \
-    return launch(kPhaseReduce, score_reduce_kernel<NARROW, VEC>, dim3(grid), dim3(256), stream, \
+    // Tags are at most V (a precondition): tag + 1 <= V + 1.
+    const int mode = (int64_t)V < (1 << 15) - 1 ? kPacked : ((int64_t)V < (1 << 24) - 1 ? kNarrow : kWideTags);
+#define PACE_REDUCE(MODE, VEC)                                                              \
+    return launch(kPhaseReduce, score_reduce_kernel<MODE, VEC>, dim3(grid), dim3(256), stream, \
                   tags, offsets, n, n_tokens, chunk_len, ch, ws.part_sum, ws.part_cnt,         \
                   ws.carry_sum, ws.carry_cnt)
-    if (narrow && vec_ok) PACE_REDUCE(true, true);
-    if (narrow) PACE_REDUCE(true, false);
-    if (vec_ok) PACE_REDUCE(false, true);
-    PACE_REDUCE(false, false);
+    if (mode == kPacked && vec_ok) PACE_REDUCE(kPacked, true);
+    if (mode == kPacked) PACE_REDUCE(kPacked, false);
+    if (mode == kNarrow && vec_ok) PACE_REDUCE(kNarrow, true);
+    if (mode == kNarrow) PACE_REDUCE(kNarrow, false);
+    if (vec_ok) PACE_REDUCE(kWideTags, true);
+    PACE_REDUCE(kWideTags, false);
 #undef PACE_REDUCE
 }
 

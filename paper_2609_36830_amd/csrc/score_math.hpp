@@ -30,11 +30,11 @@ struct TrajPieces {
 };
 
 // Chunk holding token position p >= 0. The chunk length is a multiple of
-// kScoreChunkAlign = 2^11, so p / chunk_len = (p >> 11) / (chunk_len >> 11);
-// with narrow (every position below 2^43) that is a 32-bit division.
+// kScoreChunkAlign = 2^8, so p / chunk_len = (p >> 8) / (chunk_len >> 8);
+// with narrow (every position below 2^40) that is a 32-bit division.
 __device__ __forceinline__ int64_t chunk_of(int64_t p, int64_t chunk_len, bool narrow) {
-    static_assert(kScoreChunkAlign == 2048, "chunk lengths are multiples of 2^11");
-    if (narrow) return (int64_t)((uint32_t)(p >> 11) / (uint32_t)(chunk_len >> 11));
+    static_assert(kScoreChunkAlign == 256, "chunk lengths are multiples of 2^8");
+    if (narrow) return (int64_t)((uint32_t)(p >> 8) / (uint32_t)(chunk_len >> 8));
     return p / chunk_len;
 }
 
