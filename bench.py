@@ -165,8 +165,10 @@ def reduce_traffic(config, cols):
 
 # config -> {"sha256": digest of the score_reduce sources, "bytes": HBM bytes per launch}
 REDUCE_COUNTERS = {
-    # profiles/score_reduce_stress_hbm_counters.md: FETCH_SIZE 98152.6 KiB, WRITE_SIZE 175.7 KiB
-    "stress": {"sha256": "f08e39fb9827a71d47a05d77e52064ab4794caa43ed46ea0bc13f540b3d8af53", "bytes": 201196442},
+    # profiles/filter_step_hbm_counters.md: FETCH_SIZE 98216.9 KiB, WRITE_SIZE 170.3 KiB
+    "stress": {"sha256": "6b5c5dfd5e03cd9fd343fb9ff0ba575baf1ca44aab45fa50b70d3c78ff25f158", "bytes": 201322598},
+    # profiles/filter_step_hbm_counters.md: FETCH_SIZE 103519.3 KiB, WRITE_SIZE 1138.9 KiB
+    "wide": {"sha256": "6b5c5dfd5e03cd9fd343fb9ff0ba575baf1ca44aab45fa50b70d3c78ff25f158", "bytes": 213173760},
 }
 
 
