@@ -245,6 +245,22 @@ def test_large_versions_take_the_wide_path(pace, fused):
 
 
 @FUSED
+@pytest.mark.parametrize("V", [32766, 32767, 2 ** 24 - 2, 2 ** 24 - 1])
+def test_reduce_mode_limits(pace, V, fused):
+    """Every tag at V, next to the limits where the reduction changes its
+    arithmetic (packed 2^15, 32-bit 2^24): full windows of the largest tags
+    must neither carry into the packed count nor overflow a 32-bit window
+    sum. Lengths put offsets at window edges and many windows inside one
+    trajectory; a tenth of the tokens are masked."""
+    lens = [70000, 1, 255, 256, 257, 3000, 0, 4096, 12345, 2047, 2049] + [300] * 40
+    pool = poolgen.make_custom_pool(lens, V=V, seed=V % 1000, mask_frac=0.1, c_lag=0, W=64)
+    pool.tags[:] = np.where(pool.tags == -1, -1, V).astype(np.int32)
+    pool.completion[:] = V
+    say("reduce limits V=%d fused %s" % (V, fused))
+    assert_same(gpu_step(pace, pool, fused=fused), oracle_step(pool), "V=%d" % V)
+
+
+@FUSED
 def test_large_versions_many_boundaries(pace, fused):
     """64-bit window prefixes: short trajectories put boundaries in most
     blocks of the reduction while tag + 1 reaches 2^30."""
