@@ -136,3 +136,43 @@ def test_wide_select_beyond_limit(pace):
     say("select n=%d" % n)
     for b in (1, n // 2, n - 1):
         _select_both(pace, sc, b, "beyond")
+
+
+@FUSED
+def test_wide_multi_column_payload(pace, fused):
+    """Blocks of 64 with every column width: int32 and fp32 columns copy by
+    16-byte slots, the uint8 and int16 ones element by element, fp64 and
+    int64 by slots of two elements."""
+    pool = poolgen.make_pool("wide", n=20000, seed=9)
+    rng = np.random.default_rng(9)
+    N = pool.n_tokens
+    cols = [pool.tags, rng.integers(0, 150000, N).astype(np.int32), rng.standard_normal(N).astype(np.float32),
+            (pool.tags != -1).astype(np.uint8), (np.arange(N) % 30000).astype(np.int16), rng.standard_normal(N),
+            rng.integers(-2 ** 62, 2 ** 62, N, dtype=np.int64)]
+    say("wide multi-column n=%d tokens=%d fused %s" % (pool.n, N, fused))
+    assert_same(gpu_step(pace, pool, cols=cols, fused=fused), oracle_step(pool, cols=cols), "wide multi-column")
+
+
+def test_wide_unaligned_columns(pace):
+    """Column pointers off 16-byte alignment take the element slots."""
+    pool = poolgen.make_pool("wide", n=12000, seed=13)
+    r = oracle_step(pool)
+    N = pool.n_tokens
+    rng = np.random.default_rng(13)
+    host = [rng.integers(-2 ** 31, 2 ** 31 - 1, N).astype(np.int32), rng.standard_normal(N)]
+    cols = []
+    for h in host:
+        big = torch.empty(N + 1, dtype=torch.from_numpy(h[:1]).dtype, device="cuda:0")
+        big[1:] = D(h)
+        cols.append(big[1:])
+        assert cols[-1].data_ptr() % 16 != 0
+    say("wide unaligned columns n=%d tokens=%d" % (pool.n, N))
+    oo, ids, nkt, packed = pace.pace_compact(D(pool.offsets), D(r["keep"]), cols, n_tokens=N)
+    torch.cuda.synchronize()
+    nk = int(H(nkt)[0])
+    assert nk == r["n_kept_tokens"]
+    keep = r["keep"].astype(bool)
+    spans = [np.arange(pool.offsets[i], pool.offsets[i + 1]) for i in range(pool.n) if keep[i]]
+    idx = np.concatenate(spans) if spans else np.empty(0, np.int64)
+    for h, p in zip(host, packed):
+        assert np.array_equal(H(p)[:nk], h[idx])
