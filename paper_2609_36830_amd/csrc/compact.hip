@@ -27,14 +27,9 @@
 // many workgroups, long enough that the per-workgroup set-up is small next to
 // the copy.
 //
-// Wide blocks (kWideBlock = 64 trajectories, pools up to kWideMaxN): the kept
-// spans of a block are mostly short, so one span per piece would leave every
-// piece workgroup mostly set-up. Spans longer than kPieceLen still make
-// pieces; the shorter ones of a block are copied together as segments of
-// kSegLen tokens: the block's own workgroup copies the first right after its
-// index outputs, piece workgroups the rest. A segment copy lays a table of
-// 16-byte destination slots over its spans in LDS, so each thread keeps
-// several loads in flight whatever the span lengths.
+// Wide path (8192 < n <= kWideMaxN): blocks of kWideBlock trajectories with
+// two-level partials, and the packed output split evenly over one resident
+// round of workgroups by merge path (compact_wide_kernel below).
 //
 // Scan path (larger pools): one workgroup scans the flags into the packed
 // offsets, kept ids, span sources and a map from each output chunk of
@@ -222,7 +217,7 @@ __device__ __forceinline__ int64_t kept_span(const int64_t *__restrict__ off, co
 }
 
 // One wave per block of kBlk trajectories: the block partials from the keep
-// flags (pieces as wide_block_pieces counts them for wide blocks).
+// flags.
 template <int kBlk>
 __global__ __launch_bounds__(kWave) void compact_partials_kernel(const int64_t *__restrict__ off, int64_t n,
                                                                 int64_t NT, const uint8_t *__restrict__ keep,
@@ -238,10 +233,7 @@ __global__ __launch_bounds__(kWave) void compact_partials_kernel(const int64_t *
     }
     const uint32_t c = (uint32_t)__popcll(ballot(kept));
     const int64_t l = wave_sum_i64(len);
-    const int64_t pc = kBlk == kWideBlock
-        ? wide_block_pieces(wave_sum_i64(len > kPieceLen ? (len + kPieceLen - 1) / kPieceLen : 0),
-                            wave_sum_i64(len > kPieceLen ? 0 : len))
-        : wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
+    const int64_t pc = wave_sum_i64((len + kPieceLen - 1) / kPieceLen);
     if (lane == 0) {
         parts.cnt[blockIdx.x] = (int32_t)c;
         parts.len[blockIdx.x] = l;
@@ -282,117 +274,6 @@ __device__ __forceinline__ void copy_piece(const char *__restrict__ in, char *__
     for (int64_t p = d + t; p < d + m; p += kPT) dst[p] = src[p + delta];
 }
 
-// The workgroup copies one segment of a wide block: lane j of wave 0 brings
-// destination range [a, b) of span j (empty when span j has no part in the
-// segment) and del = source - destination, in elements. The slots are, for
-// columns of 4- or 8-byte elements with 16-byte aligned pointers, the aligned
-// 16-byte destination vectors inside each range (in bytes; sources are at
-// least 4-byte aligned), else single elements; a segment has at most kSegLen
-// elements. The slots' prefix over the spans goes to LDS; each thread takes
-// slots t, t + kPT, ... (kSegU loads in flight, each slot's span by a
-// six-step binary search), and with vectors the lanes of wave 0 copy the few
-// bytes at their range's ends.
-constexpr int kSegU = 8;
-struct SegTable {
-    int32_t start[kWave + 1];   // first slot of each span; [kWave] = slots in the segment
-    int64_t dst[kWave];         // destination of each span's first slot (bytes or elements)
-    int64_t src[kWave];         // its source
-};
-
-// Span j holding slot g.
-__device__ __forceinline__ int seg_find(const SegTable &tb, int32_t g) {
-    int j = 0;
-#pragma unroll
-    for (int step = kWave / 2; step > 0; step >>= 1) j = tb.start[j + step] <= g ? j + step : j;
-    return j;
-}
-
-// Builds the slot table (wave 0) from per-lane ranges [a, b) in units of
-// `unit` and source shift del; slots are groups of `per` units at multiples
-// of `per`, units outside them go through `edge` (called by the lane).
-template <typename Edge>
-__device__ __forceinline__ void seg_table(SegTable &tb, int64_t a, int64_t b, int64_t del, int per, Edge edge) {
-    int64_t v0 = (a + per - 1) / per, v1 = b / per;
-    if (v1 < v0) v1 = v0;
-    const int32_t cnt = (int32_t)(v1 - v0);
-    const int32_t incl = (int32_t)wave_incl_scan_u32((uint32_t)cnt);
-    const int t = threadIdx.x;
-    tb.start[t] = incl - cnt;
-    if (t == kWave - 1) tb.start[kWave] = incl;
-    tb.dst[t] = v0 * per;
-    tb.src[t] = v0 * per + del;
-    const int64_t h = cnt > 0 ? v0 * per : b;
-    for (int64_t p = a; p < h; ++p) edge(p);
-    if (cnt > 0)
-        for (int64_t p = v1 * per; p < b; ++p) edge(p);
-}
-
-// 16-byte vector slots over byte ranges.
-__device__ void copy_segment_vec(const char *__restrict__ in, char *__restrict__ out, int64_t a, int64_t b,
-                                 int64_t del, SegTable &tb) {
-    const int t = threadIdx.x;
-    __syncthreads();                           // the previous column's table is no longer read
-    if (t < kWave) seg_table(tb, a, b, del, 16, [&](int64_t p) { out[p] = in[p + del]; });
-    __syncthreads();
-    const int32_t total = tb.start[kWave];
-    for (int32_t g0 = t; g0 < total; g0 += kSegU * kPT) {
-        uint32_t jr[kSegU];                    // span << 26 | slot in span; ~0: none
-        uint4 x[kSegU];
-#pragma unroll
-        for (int u = 0; u < kSegU; ++u) {
-            const int32_t g = g0 + u * kPT;
-            jr[u] = ~0u;
-            if (g < total) {
-                const int j = seg_find(tb, g);
-                const int32_t r = g - tb.start[j];
-                jr[u] = ((uint32_t)j << 26) | (uint32_t)r;
-                x[u] = load_a4(in + tb.src[j] + (int64_t)r * 16);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < kSegU; ++u)
-            if (jr[u] != ~0u)
-                store_nt(reinterpret_cast<uint4 *>(out + tb.dst[jr[u] >> 26] + (int64_t)(jr[u] & 0x3ffffffu) * 16),
-                         x[u]);
-    }
-}
-
-// Single-element slots.
-template <int E>
-__device__ void copy_segment_elem(const char *__restrict__ in, char *__restrict__ out, int64_t a, int64_t b,
-                                  int64_t del, SegTable &tb) {
-    using T = typename Elem<E>::T;
-    const T *src = reinterpret_cast<const T *>(in);
-    T *dst = reinterpret_cast<T *>(out);
-    const int t = threadIdx.x;
-    __syncthreads();
-    if (t < kWave) seg_table(tb, a, b, del, 1, [&](int64_t) {});
-    __syncthreads();
-    const int32_t total = tb.start[kWave];
-    for (int32_t g = t; g < total; g += kPT) {
-        const int j = seg_find(tb, g);
-        const int64_t r = g - tb.start[j];
-        dst[tb.dst[j] + r] = src[tb.src[j] + r];
-    }
-}
-
-__device__ __forceinline__ void copy_segment_col(const CompactCols &cols, int col, int64_t a, int64_t b, int64_t del,
-                                                 SegTable &tb) {
-    const char *in = (const char *)cols.in[col];
-    char *out = (char *)cols.out[col];
-    const int E = cols.elem[col];
-    if (cols.vec[col] != 0 && E >= 4) {
-        copy_segment_vec(in, out, a * E, b * E, del * E, tb);
-        return;
-    }
-    switch (E) {
-        case 1: copy_segment_elem<1>(in, out, a, b, del, tb); break;
-        case 2: copy_segment_elem<2>(in, out, a, b, del, tb); break;
-        case 4: copy_segment_elem<4>(in, out, a, b, del, tb); break;
-        default: copy_segment_elem<8>(in, out, a, b, del, tb); break;
-    }
-}
-
 // kBlk trajectories per block (at most a wave); thread t holds the partials
 // of blocks [t*kPP, (t+1)*kPP). offsets_out, kept_ids and n_kept_tokens may
 // be null (rejected ids only).
@@ -413,21 +294,6 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
     if (t == 0) {
         sel[0] = sel[1] = sel[2] = 0;
         piece[0] = piece[1] = piece[2] = 0;   // an unmatched piece copies nothing
-    }
-    // Wide block workgroups: the block's spans, loaded with the partials
-    // (flag and offsets together: one round trip). len -1: rejected.
-    int64_t b_lo = 0, b_len = -1;
-    if constexpr (kBlk == kWideBlock) {
-        const int64_t i = q * kBlk + t;
-        if (q < nb && t < kWave && i < n) {
-            const uint8_t kf = keep[i];
-            const int64_t a = off[i], b = off[i + 1];
-            if (kf != 0) {
-                b_lo = clamp64(a, 0, NT);
-                const int64_t hi = clamp64(b, 0, NT);
-                b_len = hi > b_lo ? hi - b_lo : 0;
-            }
-        }
     }
 
     // 1. Exclusive prefix of the block partials; thread t holds blocks
@@ -468,17 +334,12 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
             lb += l[k];
         }
         __syncthreads();
-        int64_t a = 0, e = 0, del = 0;         // wide: span t's part of the block's first segment
         if (t < kWave) {
             const int64_t i = q * kBlk + t;
             const bool in = t < kBlk && i < n;
-            int64_t len = 0, lo = 0;
+            int64_t len = 0, lo;
             bool kept = false;
-            if constexpr (kBlk == kWideBlock) {
-                kept = b_len >= 0;
-                len = kept ? b_len : 0;
-                lo = b_lo;
-            } else if (in) {
+            if (in) {
                 const int64_t k = kept_span(off, keep, i, NT, lo);
                 kept = k >= 0;
                 len = kept ? k : 0;
@@ -494,130 +355,13 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
                 const int64_t rr = i - rank;       // trajectories before i that were rejected
                 if (rr < budget) reject_ids[rr] = (int32_t)i;
             }
-            if constexpr (kBlk == kWideBlock) {
-                const int64_t sl = len > kPieceLen ? 0 : len;
-                const int64_t f = wave_incl_scan_i64(sl) - sl;
-                const int64_t fb = (f + sl < kSegLen) ? f + sl : kSegLen;
-                if (fb > f) {
-                    a = dst;
-                    e = dst + (fb - f);
-                    del = lo - dst;
-                    if (e > NT) e = NT;                // overlapping (malformed) offsets overflow the output
-                    if (a > e) a = e;
-                }
-            }
-        }
-        if constexpr (kBlk == kWideBlock) {
-            __shared__ SegTable tb0;
-            for (int col = 0; col < n_cols; ++col) copy_segment_col(cols, col, a, e, del, tb0);
         }
         return;
     }
 
     // 2b. Pieces q - nb, q - nb + stride, ... (stride = piece workgroups in
-    //     the grid): for each, its block, then its trajectory in the block
-    //     (wide blocks: a piece of a long span, or a segment of the short ones
-//     after the first, which the block's workgroup copies).
+    //     the grid): for each, its block, then its trajectory in the block.
     const int64_t stride = (int64_t)gridDim.x - nb;
-    if constexpr (kBlk == kWideBlock) {
-        __shared__ SegTable tb;
-        __shared__ int sg_mode;
-        // The blocks' piece and token prefixes move to LDS, so that no
-        // register holds them while the pieces are copied.
-        __shared__ uint32_t s_pb[kPT * kPartsPerThread + 1];
-        __shared__ int64_t s_lb[kPT * kPartsPerThread];
-        {
-            uint32_t pbk = pb;
-            int64_t lbk = lb;
-#pragma unroll
-            for (int k = 0; k < kPartsPerThread; ++k) {
-                s_pb[t * kPartsPerThread + k] = pbk;
-                s_lb[t * kPartsPerThread + k] = lbk;
-                pbk += pc[k];
-                lbk += l[k];
-            }
-            if (t == kPT - 1) s_pb[kPT * kPartsPerThread] = pbk;
-        }
-        for (int64_t pq = q - nb; pq < (int64_t)tot_p; pq += stride) {
-            __syncthreads();                   // the previous piece's reads of sel/piece/sg_mode are done
-            if (t == 0) {
-                sel[0] = sel[1] = sel[2] = 0;
-                piece[0] = piece[1] = piece[2] = 0;
-                sg_mode = 0;
-            }
-            __syncthreads();
-#pragma unroll
-            for (int k = 0; k < kPartsPerThread; ++k) {
-                const int b = t * kPartsPerThread + k;
-                const uint32_t p0 = s_pb[b], p1 = s_pb[b + 1];
-                if (b < nb && (int64_t)p0 <= pq && pq < (int64_t)p1) {
-                    sel[0] = b;
-                    sel[1] = p0;
-                    sel[2] = s_lb[b];
-                }
-            }
-            __syncthreads();
-            int64_t a = 0, e = 0, del = 0;     // wave 0, lane j: span j's destination range and shift
-            if (t < kWave) {
-                const int64_t i = sel[0] * kBlk + t;
-                int64_t len = 0, lo = 0;
-                if (i < n) {
-                    const int64_t k = kept_span(off, keep, i, NT, lo);
-                    len = k > 0 ? k : 0;
-                }
-                const int64_t dst = sel[2] + (wave_incl_scan_i64(len) - len);
-                const bool lng = len > kPieceLen;
-                const int64_t np = lng ? (len + kPieceLen - 1) / kPieceLen : 0;
-                const int64_t np_incl = wave_incl_scan_i64(np);
-                const int64_t n_long = readlane_i64(np_incl, kWave - 1);
-                const int64_t qq = pq - sel[1];
-                if (qq < n_long) {
-                    if (np > 0 && np_incl - np <= qq && qq < np_incl) {
-                        const int64_t k = qq - (np_incl - np);
-                        piece[0] = dst + k * kPieceLen;
-                        piece[1] = lo + k * kPieceLen;
-                        piece[2] = (len - k * kPieceLen) < kPieceLen ? len - k * kPieceLen : kPieceLen;
-                    }
-                    if (t == 0) sg_mode = 1;
-                } else {
-                    const int64_t sl = lng ? 0 : len;
-                    const int64_t f = wave_incl_scan_i64(sl) - sl;     // span's start among the short tokens
-                    const int64_t s0 = (qq - n_long + 1) * kSegLen, s1 = s0 + kSegLen;
-                    const int64_t fa = f > s0 ? f : s0, fb = (f + sl < s1) ? f + sl : s1;
-                    if (fb > fa) {
-                        a = dst + (fa - f);
-                        e = dst + (fb - f);
-                        del = lo - dst;
-                        if (e > NT) e = NT;            // overlapping (malformed) offsets overflow the output
-                        if (a > e) a = e;
-                    }
-                    if (t == 0) sg_mode = 2;
-                }
-            }
-            __syncthreads();
-            const int mode = sg_mode;
-            if (mode == 2) {
-                for (int col = 0; col < n_cols; ++col) copy_segment_col(cols, col, a, e, del, tb);
-                continue;
-            }
-            const int64_t d = piece[0], s = piece[1];
-            int64_t m = piece[2];
-            if (mode != 1 || d >= NT || m <= 0) continue;
-            if (d + m > NT) m = NT - d;
-            for (int col = 0; col < n_cols; ++col) {
-                const char *in = (const char *)cols.in[col];
-                char *out = (char *)cols.out[col];
-                const bool vec = cols.vec[col] != 0;
-                switch (cols.elem[col]) {
-                    case 1: copy_piece<1>(in, out, vec, d, s, m); break;
-                    case 2: copy_piece<2>(in, out, vec, d, s, m); break;
-                    case 4: copy_piece<4>(in, out, vec, d, s, m); break;
-                    default: copy_piece<8>(in, out, vec, d, s, m); break;
-                }
-            }
-        }
-        return;
-    }
     for (int64_t pq = q - nb; pq < (int64_t)tot_p; pq += stride) {
         __syncthreads();                       // the previous piece's reads of sel/piece are done
         if (t == 0) {
@@ -673,6 +417,374 @@ __global__ __launch_bounds__(kPT) void compact_piece_kernel(
                 case 4: copy_piece<4>(in, out, vec, d, s, m); break;
                 default: copy_piece<8>(in, out, vec, d, s, m); break;
             }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Wide path: blocks of kWideBlock trajectories, the copy split by merge path
+// ---------------------------------------------------------------------------
+// The block partials come in two levels: per block (kept count and tokens)
+// and per group of kGroupBlocks blocks (their sums), so that a workgroup
+// finds any block's packed position from at most kWideMaxGroups group sums
+// and the kGroupBlocks - 1 blocks before it in its group, with wave
+// reductions and no scan over all blocks.
+//
+// The packed output is split evenly by a merge path over the cost (kept
+// tokens + kBlockCost per block): workgroup q copies the kept tokens of cost
+// range [q S, (q + 1) S), S = ceil(total cost / grid), which holds at most
+// S / kBlockCost + 2 blocks, four blocks (one per wave) at a time. Then wave w
+// of workgroup q writes the index outputs of block q + w * grid.
+constexpr int64_t kBlockCost = 2048;
+constexpr int kSpanT = kPT;               // spans in one copy table: four blocks of one wave each
+constexpr int kSpanU = 8;                 // 16-byte loads in flight per thread in a span copy
+struct SpanTable {
+    int32_t start[kSpanT + 1];   // first slot of each span; [kSpanT] = slots in the table
+    int64_t dst[kSpanT];         // destination of each span's first slot (bytes or elements)
+    int64_t src[kSpanT];         // its source
+};
+
+// The span holding slot g: the last span whose first slot is <= g.
+__device__ __forceinline__ int span_find(const SpanTable &tb, int32_t g) {
+    int j = 0;
+#pragma unroll
+    for (int step = kSpanT / 2; step > 0; step >>= 1) j = tb.start[j + step] <= g ? j + step : j;
+    return j;
+}
+
+// Thread t brings span t's range [a, b) and shift del (source - destination)
+// in elements; the slots are groups of `per` elements at multiples of `per`
+// inside the range, [v0, v1) the part they cover (v0 = v1 when none), so that
+// [a, v0) and [v1, b) each hold fewer than `per` elements.
+__device__ __forceinline__ void span_table(SpanTable &tb, uint32_t *wsum, int64_t a, int64_t b, int64_t del,
+                                           int per, int64_t &v0, int64_t &v1) {
+    v0 = (a + per - 1) / per * per;
+    v1 = b / per * per;
+    if (v1 < v0) v1 = v0;
+    if (v0 > b) v0 = v1 = b;
+    const uint32_t cnt = (uint32_t)((v1 - v0) / per);
+    uint32_t tot;
+    const uint32_t ex = block_excl_sum_u32<kPW>(cnt, tot, wsum);
+    const int t = threadIdx.x;
+    tb.start[t] = (int32_t)ex;
+    if (t == kPT - 1) tb.start[kSpanT] = (int32_t)tot;
+    tb.dst[t] = v0;
+    tb.src[t] = v0 + del;
+}
+
+// Columns of 4- or 8-byte elements with 16-byte aligned pointers: the slots
+// are the aligned 16-byte destination vectors (sources at least 4-byte
+// aligned, one dwordx4 load each); each thread then copies the elements at
+// its own range's ends (fewer than 16 bytes at each end, all loads first).
+template <int E>
+__device__ void copy_spans_vec(const char *__restrict__ in, char *__restrict__ out, int64_t a, int64_t b,
+                               int64_t del, SpanTable &tb, uint32_t *wsum) {
+    using T = typename Elem<E>::T;
+    constexpr int VE = 16 / E;
+    const T *src = reinterpret_cast<const T *>(in);
+    T *dst = reinterpret_cast<T *>(out);
+    const int t = threadIdx.x;
+    __syncthreads();                           // the previous table is no longer read
+    int64_t v0, v1;
+    span_table(tb, wsum, a, b, del, VE, v0, v1);
+    __syncthreads();
+    const int32_t total = tb.start[kSpanT];
+    for (int32_t g0 = t; g0 < total; g0 += kSpanU * kPT) {
+        uint4 x[kSpanU];
+#pragma unroll
+        for (int u = 0; u < kSpanU; ++u) {
+            const int32_t g = g0 + u * kPT;
+            if (g < total) {
+                const int j = span_find(tb, g);
+                x[u] = load_a4(src + tb.src[j] + (int64_t)(g - tb.start[j]) * VE);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kSpanU; ++u) {
+            const int32_t g = g0 + u * kPT;
+            if (g < total) {
+                const int j = span_find(tb, g);
+                store_nt(reinterpret_cast<uint4 *>(dst + tb.dst[j] + (int64_t)(g - tb.start[j]) * VE), x[u]);
+            }
+        }
+    }
+    T h[VE - 1], e[VE - 1];
+#pragma unroll
+    for (int k = 0; k < VE - 1; ++k) {
+        if (a + k < v0) h[k] = src[a + k + del];
+        if (v1 + k < b) e[k] = src[v1 + k + del];
+    }
+#pragma unroll
+    for (int k = 0; k < VE - 1; ++k) {
+        if (a + k < v0) dst[a + k] = h[k];
+        if (v1 + k < b) dst[v1 + k] = e[k];
+    }
+}
+
+// Any other column: one element per slot.
+template <int E>
+__device__ void copy_spans_elem(const char *__restrict__ in, char *__restrict__ out, int64_t a, int64_t b,
+                                int64_t del, SpanTable &tb, uint32_t *wsum) {
+    using T = typename Elem<E>::T;
+    const T *src = reinterpret_cast<const T *>(in);
+    T *dst = reinterpret_cast<T *>(out);
+    const int t = threadIdx.x;
+    __syncthreads();
+    int64_t v0, v1;
+    span_table(tb, wsum, a, b, del, 1, v0, v1);
+    __syncthreads();
+    const int32_t total = tb.start[kSpanT];
+    for (int32_t g = t; g < total; g += kPT) {
+        const int j = span_find(tb, g);
+        const int64_t r = g - tb.start[j];
+        dst[tb.dst[j] + r] = src[tb.src[j] + r];
+    }
+}
+
+// Range [a, b) of a column, shift del, in elements.
+__device__ __forceinline__ void copy_spans_col(const CompactCols &cols, int col, int64_t a, int64_t b, int64_t del,
+                                               SpanTable &tb, uint32_t *wsum) {
+    const char *in = (const char *)cols.in[col];
+    char *out = (char *)cols.out[col];
+    const bool vec = cols.vec[col] != 0;
+    switch (cols.elem[col]) {
+        case 1: copy_spans_elem<1>(in, out, a, b, del, tb, wsum); break;
+        case 2: copy_spans_elem<2>(in, out, a, b, del, tb, wsum); break;
+        case 4:
+            if (vec) copy_spans_vec<4>(in, out, a, b, del, tb, wsum);
+            else copy_spans_elem<4>(in, out, a, b, del, tb, wsum);
+            break;
+        default:
+            if (vec) copy_spans_vec<8>(in, out, a, b, del, tb, wsum);
+            else copy_spans_elem<8>(in, out, a, b, del, tb, wsum);
+            break;
+    }
+}
+
+// Inclusive scan inside each row of 16 lanes (row_shr 1, 2, 4, 8).
+__device__ __forceinline__ int64_t row_incl_scan_i64(int64_t v) {
+    auto add = [](uint64_t a, uint64_t b) { return a + b; };
+    uint64_t x = (uint64_t)v;
+    x = add(x, dpp_u64<0x111, 0xf>(0ull, x));
+    x = add(x, dpp_u64<0x112, 0xf>(0ull, x));
+    x = add(x, dpp_u64<0x114, 0xf>(0ull, x));
+    x = add(x, dpp_u64<0x118, 0xf>(0ull, x));
+    return (int64_t)x;
+}
+
+// One workgroup of 1024 threads per kGroupBlocks blocks of kWideBlock
+// trajectories (one wave each): the block partials from the keep flags and
+// the group's sums.
+__global__ __launch_bounds__(kWideBlock * kGroupBlocks) void compact_partials_wide_kernel(
+    const int64_t *__restrict__ off, int64_t n, int64_t NT, const uint8_t *__restrict__ keep, PieceParts parts) {
+    static_assert(kWideBlock == kWave, "a wide block is one wave");
+    __shared__ uint32_t sc[kGroupBlocks];
+    __shared__ int64_t sl[kGroupBlocks];
+    const int lane = lane_id(), w = threadIdx.x / kWave;
+    const int64_t b = (int64_t)blockIdx.x * kGroupBlocks + w;
+    const int64_t i = b * kWideBlock + lane;
+    int64_t len = 0, lo;
+    bool kept = false;
+    if (i < n) {
+        const int64_t k = kept_span(off, keep, i, NT, lo);
+        kept = k >= 0;
+        len = kept ? k : 0;
+    }
+    const uint32_t c = (uint32_t)__popcll(ballot(kept));
+    const int64_t l = wave_sum_i64(len);
+    if (lane == 0) {
+        if (b * kWideBlock < n) {
+            parts.cnt[b] = (int32_t)c;
+            parts.len[b] = l;
+        }
+        sc[w] = c;
+        sl[w] = l;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t gc = 0;
+        int64_t gl = 0;
+        for (int k = 0; k < kGroupBlocks; ++k) {
+            gc += sc[k];
+            gl += sl[k];
+        }
+        parts.gcnt[blockIdx.x] = (int32_t)gc;
+        parts.glen[blockIdx.x] = gl;
+    }
+}
+
+// nb blocks in ng = ceil(nb / kGroupBlocks) <= kWideMaxGroups groups;
+// 4 * grid >= nb. offsets_out, kept_ids and n_kept_tokens may be null
+// (rejected ids only).
+__global__ __launch_bounds__(kPT) void compact_wide_kernel(
+    const int64_t *__restrict__ off, int64_t n, int64_t NT, const uint8_t *__restrict__ keep,
+    PieceParts parts, int64_t nb, CompactCols cols, int n_cols, int64_t *__restrict__ offsets_out,
+    int32_t *__restrict__ kept_ids, int64_t *__restrict__ n_kept_tokens, int32_t *__restrict__ reject_ids,
+    int64_t budget) {
+    static_assert(kWideBlock == kWave, "a wide block is one wave");
+    static_assert(kWideMaxGroups == 4 * kWave, "group sums: four per lane of one wave");
+    __shared__ int64_t s_gl[kWideMaxGroups + 1];   // kept tokens before each group; [kWideMaxGroups] = total
+    __shared__ uint32_t s_gc[kWideMaxGroups + 1];  // kept trajectories before each group
+    __shared__ int64_t s_cut[6];                   // b0, b1, x0, x1
+    __shared__ uint32_t wsum[kPW];
+    __shared__ SpanTable tb;
+    const int t = threadIdx.x, w = t / kWave, lane = lane_id();
+    const int64_t q = blockIdx.x, G = gridDim.x;
+    const int64_t ng = (nb + kGroupBlocks - 1) / kGroupBlocks;
+
+    // The block `b`'s kept count and tokens before it inside its group: the
+    // wave's lanes below kGroupBlocks hold the group's earlier blocks.
+    auto in_group = [&](int64_t b, uint32_t &c, int64_t &l) {
+        const int64_t j = b / kGroupBlocks * kGroupBlocks + lane;
+        c = 0u;
+        l = 0;
+        if (lane < kGroupBlocks && j < b) {
+            c = (uint32_t)parts.cnt[j];
+            l = parts.len[j];
+        }
+    };
+
+    // 0. The index block of this wave: its spans and its group's earlier
+    //    partials, loaded with the group sums (one round trip).
+    const int64_t ib = q + (int64_t)w * G;
+    int64_t i_lo = 0, i_len = -1;
+    uint32_t i_c = 0u;
+    int64_t i_l = 0;
+    if (ib < nb) {
+        const int64_t i = ib * kWideBlock + lane;
+        if (i < n) {
+            const uint8_t kf = keep[i];
+            const int64_t a = off[i], b = off[i + 1];
+            if (kf != 0) {
+                i_lo = clamp64(a, 0, NT);
+                const int64_t hi = clamp64(b, 0, NT);
+                i_len = hi > i_lo ? hi - i_lo : 0;
+            }
+        }
+        in_group(ib, i_c, i_l);
+    }
+
+    // 1. Exclusive prefixes of the group sums (wave 0, four groups per lane).
+    if (w == 0) {
+        uint32_t c4[4];
+        int64_t l4[4];
+        uint32_t cs = 0u;
+        int64_t ls = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int64_t g = (int64_t)lane * 4 + k;
+            c4[k] = g < ng ? (uint32_t)parts.gcnt[g] : 0u;
+            l4[k] = g < ng ? parts.glen[g] : 0;
+            cs += c4[k];
+            ls += l4[k];
+        }
+        uint32_t ce = wave_incl_scan_u32(cs) - cs;
+        int64_t le = wave_incl_scan_i64(ls) - ls;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            s_gc[lane * 4 + k] = ce;
+            s_gl[lane * 4 + k] = le;
+            ce += c4[k];
+            le += l4[k];
+        }
+        if (lane == kWave - 1) {
+            s_gc[kWideMaxGroups] = ce;
+            s_gl[kWideMaxGroups] = le;
+        }
+    }
+    __syncthreads();
+    const int64_t tot_l = s_gl[kWideMaxGroups];
+
+    // 2. Copy the kept tokens of cost range [q S, (q + 1) S). Wave 0 finds the
+    //    blocks holding costs c0, c1 - 1 and c1: per cost, a binary search over
+    //    the groups' cost starts, then lanes 16u .. 16u + 15 scan that group's
+    //    block lengths (row u of the wave).
+    const int64_t T = tot_l + kBlockCost * nb;
+    const int64_t S = (T + G - 1) / G;
+    const int64_t c0 = q * S;
+    if (n_cols > 0 && nb > 0 && c0 < T) {
+        const int64_t c1 = (c0 + S < T) ? c0 + S : T;
+        if (w == 0) {
+            const int u = lane / kGroupBlocks, r = lane % kGroupBlocks;
+            const int64_t key = u == 0 ? c0 : (u == 1 ? c1 - 1 : c1);
+            int64_t lo = 0, hi = ng;                // last group whose cost starts at or before key
+            while (hi - lo > 1) {
+                const int64_t mid = (lo + hi) / 2;
+                if (s_gl[mid] + kBlockCost * kGroupBlocks * mid <= key) lo = mid;
+                else hi = mid;
+            }
+            const int64_t j = lo * kGroupBlocks + r;
+            const int64_t len = (u < 3 && j < nb) ? parts.len[j] : 0;
+            const int64_t before = s_gl[lo] + (row_incl_scan_i64(len) - len);
+            const int64_t cst = before + kBlockCost * j;   // cost start of block j
+            const bool ok = u < 3 && j < nb && cst <= key;
+            const uint64_t m = ballot(ok);
+            const uint32_t row = (uint32_t)(m >> (16 * u)) & 0xffffu;
+            const bool last = ok && (row >> (r + 1)) == 0u;
+            if (last) {
+                if (u == 0) s_cut[0] = j;
+                if (u == 1) s_cut[1] = j;
+                const int64_t rr = key - cst - kBlockCost;
+                const int64_t x = before + (rr < 0 ? 0 : (rr > len ? len : rr));
+                if (u == 0) s_cut[2] = x;
+                if (u == 2) s_cut[3] = x;
+            }
+        }
+        __syncthreads();
+        const int64_t b0 = s_cut[0], b1 = s_cut[1], x0 = s_cut[2], x1 = s_cut[3];
+        for (int64_t bg = b0; x0 < x1 && bg <= b1; bg += kPW) {
+            // Wave w: block bg + w, lane j its trajectory j; the part of its
+            // kept span inside [x0, x1).
+            const int64_t b = bg + w;
+            int64_t a = 0, e = 0, del = 0;
+            if (b <= b1) {
+                const int64_t i = b * kWideBlock + lane;
+                int64_t len = 0, lo_i = 0;
+                if (i < n) {
+                    const int64_t k = kept_span(off, keep, i, NT, lo_i);
+                    len = k > 0 ? k : 0;
+                }
+                uint32_t gc;
+                int64_t gl;
+                in_group(b, gc, gl);
+                const int64_t lb = s_gl[b / kGroupBlocks] + wave_sum_i64(gl);
+                const int64_t dst = lb + (wave_incl_scan_i64(len) - len);
+                const int64_t s0 = dst > x0 ? dst : x0;
+                const int64_t s1 = (dst + len < x1) ? dst + len : x1;
+                if (s1 > s0) {
+                    a = s0;
+                    e = s1 < NT ? s1 : NT;             // overlapping (malformed) offsets overflow the output
+                    if (a > e) a = e;
+                    del = lo_i - dst;
+                }
+            }
+            for (int col = 0; col < n_cols; ++col) copy_spans_col(cols, col, a, e, del, tb, wsum);
+        }
+    }
+
+    // 3. Index outputs of block ib (after the copy: their stores would hold
+    //    up the copy's first loads, one counter covering both).
+    if (q == 0 && t == 0 && offsets_out) {
+        offsets_out[s_gc[kWideMaxGroups]] = tot_l;
+        *n_kept_tokens = tot_l;
+    }
+    if (ib < nb) {
+        const int64_t i = ib * kWideBlock + lane;
+        const bool kept = i_len >= 0;
+        const int64_t len = kept ? i_len : 0;
+        const int64_t g = ib / kGroupBlocks;
+        const int64_t cb = (int64_t)s_gc[g] + (int64_t)wave_sum_u64((uint64_t)i_c);
+        const int64_t lb = s_gl[g] + wave_sum_i64(i_l);
+        const int64_t rank = cb + (int64_t)__popcll(ballot(kept) & lanes_below());
+        const int64_t dst = lb + (wave_incl_scan_i64(len) - len);
+        if (kept) {
+            if (offsets_out) {
+                offsets_out[rank] = dst;
+                kept_ids[rank] = (int32_t)i;
+            }
+        } else if (i < n && reject_ids) {
+            const int64_t rr = i - rank;           // trajectories before i that were rejected
+            if (rr < budget) reject_ids[rr] = (int32_t)i;
         }
     }
 }
@@ -757,14 +869,18 @@ CompactWs compact_ws_carve(void *ws, int64_t n, int64_t n_tokens) {
     w.chunk_first = (int32_t *)p;  p += align256((size_t)map_capacity(n_tokens) * 4);
     w.parts.cnt = (int32_t *)p;    p += align256(nb * 4);
     w.parts.len = (int64_t *)p;    p += align256(nb * 8);
-    w.parts.pcs = (int32_t *)p;
+    w.parts.pcs = (int32_t *)p;    p += align256(nb * 4);
+    const size_t ng = (size_t)wide_groups(n);
+    w.parts.gcnt = (int32_t *)p;   p += align256(ng * 4);
+    w.parts.glen = (int64_t *)p;
     return w;
 }
 
 size_t compact_ws_bytes(int64_t n, int64_t n_tokens) {
     const size_t nb = (size_t)piece_blocks(n);
+    const size_t ng = (size_t)wide_groups(n);
     return 256 + align256((size_t)n * 8) + align256((size_t)map_capacity(n_tokens) * 4) +
-           align256(nb * 4) * 2 + align256(nb * 8);
+           align256(nb * 4) * 2 + align256(nb * 8) + align256(ng * 4) + align256(ng * 8);
 }
 
 bool compact_piece_ok(int64_t n, int64_t n_tokens) {
@@ -780,8 +896,9 @@ hipError_t launch_compact_partials(const int64_t *offsets, int64_t n, int64_t n_
                                    int blk) {
     if (n == 0) return hipSuccess;
     if (blk == kWideBlock)
-        return launch(-1, compact_partials_kernel<kWideBlock>, dim3((unsigned)((n + kWideBlock - 1) / kWideBlock)),
-                      dim3(kWave), stream, offsets, n, n_tokens, keep, parts);
+        return launch(-1, compact_partials_wide_kernel,
+                      dim3((unsigned)((n + kWideBlock * kGroupBlocks - 1) / (kWideBlock * kGroupBlocks))),
+                      dim3(kWideBlock * kGroupBlocks), stream, offsets, n, n_tokens, keep, parts);
     return launch(-1, compact_partials_kernel<kPieceBlock>, dim3((unsigned)piece_blocks(n)), dim3(kWave), stream,
                   offsets, n, n_tokens, keep, parts);
 }
@@ -812,12 +929,15 @@ hipError_t launch_compact_pieces(const int64_t *offsets, int64_t n, int64_t n_to
         if (per > 2) return hipErrorInvalidValue;
         PACE_PIECES(kPieceBlock, 2);
     }
-    if (blk != kWideBlock || per > 16) return hipErrorInvalidValue;
-    if (per <= 2) PACE_PIECES(kWideBlock, 2);
-    if (per <= 4) PACE_PIECES(kWideBlock, 4);
-    if (per <= 8) PACE_PIECES(kWideBlock, 8);
-    PACE_PIECES(kWideBlock, 16);
 #undef PACE_PIECES
+    if (blk != kWideBlock || (nb + kGroupBlocks - 1) / kGroupBlocks > kWideMaxGroups) return hipErrorInvalidValue;
+    // Every workgroup indexes up to four blocks and copies an even share of
+    // the output: one resident round (four per CU) when copying.
+    int64_t wgs = (nb + kPW - 1) / kPW;
+    if (copy && wgs < resident_waves() / 16 * 4) wgs = resident_waves() / 16 * 4;
+    if (wgs < 1) wgs = 1;
+    return launch(kPhaseCompact, compact_wide_kernel, dim3((unsigned)wgs), dim3(kPT), stream, offsets, n, n_tokens,
+                  keep, parts, nb, cols, copy ? n_cols : 0, offsets_out, kept_ids, n_kept_tokens, reject_ids, budget);
 }
 
 hipError_t launch_compact_copy(const CompactCols &cols, int n_cols, int64_t n_tokens,

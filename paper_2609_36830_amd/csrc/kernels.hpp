@@ -113,7 +113,9 @@ constexpr int64_t kPieceMaxN = 8192;   // at most 512 blocks
 struct PieceParts {
     int32_t *cnt;
     int64_t *len;
-    int32_t *pcs;
+    int32_t *pcs;      // blocks of kPieceBlock only
+    int32_t *gcnt;     // wide blocks only: per group of kGroupBlocks blocks, the sums of cnt and len
+    int64_t *glen;
 };
 inline int64_t piece_blocks(int64_t n) { return (n + kPieceBlock - 1) / kPieceBlock; }
 
@@ -127,16 +129,11 @@ struct CutRec {
     int64_t pad;
 };
 constexpr int kWideBlock = 64;          // trajectories per compaction block on the wide path
-// Pieces of a wide block: each kept span longer than kPieceLen is cut into
-// ceil(len / kPieceLen) pieces; the shorter kept spans, taken together in
-// block order, into segments of kSegLen tokens (the last one shorter), of
-// which the block's own workgroup copies the first.
-constexpr int64_t kSegLen = 24576;
-__host__ __device__ inline int64_t wide_block_pieces(int64_t long_pieces, int64_t short_tokens) {
-    return long_pieces + (short_tokens > 0 ? (short_tokens - 1) / kSegLen : 0);
-}
+constexpr int kGroupBlocks = 16;        // wide blocks per group of the two-level block partials
 constexpr int64_t kWideHistMax = 64;    // histogram workgroups
-constexpr int64_t kWideMaxN = 262144;   // piece compaction limit with wide blocks
+constexpr int64_t kWideMaxN = 262144;   // limit of the wide selection and compaction
+constexpr int kWideMaxGroups = (int)(kWideMaxN / (kWideBlock * kGroupBlocks));
+inline int64_t wide_groups(int64_t n) { return (n + kWideBlock * kGroupBlocks - 1) / (kWideBlock * kGroupBlocks); }
 constexpr int kCutBits = 11;           // level-0 digits of the cut search: 2^kCutBits bins
 struct WideWs {
     CutRec *cut;

@@ -26,8 +26,9 @@
 //               ordered count. More candidates than LDS holds are refined by
 //               histogramming the scores again from global memory.
 //               Then one thread per trajectory applies the cut: keep flags,
-//               and per block of kWideBlock trajectories the kept count, kept
-//               tokens and piece count the piece compaction consumes.
+//               per block of kWideBlock trajectories the kept count and kept
+//               tokens, and their sums per group of kGroupBlocks blocks, the
+//               two-level partials the wide compaction reads.
 // Histograms use LDS atomics, plus one global atomic per non-empty bin and
 // workgroup; the integer counts do not depend on their order.
 #include "device_util.hpp"
@@ -484,10 +485,10 @@ __device__ void find_cut(const double *__restrict__ score, int64_t n, int64_t bu
 }
 
 // One 1024-thread workgroup per 1024 trajectories: the cut (find_cut, the
-// same in every workgroup), then per trajectory the keep flag, and per block
-// of kWideBlock trajectories (one wave) the kept count, kept tokens (spans
-// clamped to [0, NT]) and pieces (wide_block_pieces; zero without offsets).
-// Workgroup 0 also stores the cut.
+// same in every workgroup), then per trajectory the keep flag, per block of
+// kWideBlock trajectories (one wave) the kept count and kept tokens (spans
+// clamped to [0, NT]; zero without offsets), and per workgroup (a group of
+// kGroupBlocks blocks) their sums. Workgroup 0 also stores the cut.
 __global__ __launch_bounds__(kWT) void classify_kernel(const double *__restrict__ score,
                                                        const int64_t *__restrict__ off, int64_t n, int64_t NT,
                                                        int64_t budget, const uint32_t *__restrict__ hist,
@@ -520,13 +521,27 @@ __global__ __launch_bounds__(kWT) void classify_kernel(const double *__restrict_
     }
     const uint32_t kc = (uint32_t)__popcll(ballot(kept));
     const int64_t l = wave_sum_i64(len);
-    const int64_t pc = wide_block_pieces(wave_sum_i64(len > kPieceLen ? (len + kPieceLen - 1) / kPieceLen : 0),
-                                         wave_sum_i64(len > kPieceLen ? 0 : len));
     const int64_t b = i / kWideBlock;
-    if (lane_id() == 0 && b * kWideBlock < n) {
-        parts.cnt[b] = (int32_t)kc;
-        parts.len[b] = l;
-        parts.pcs[b] = (int32_t)pc;
+    const int w = threadIdx.x / kWave;
+    static_assert(kWT == kWideBlock * kGroupBlocks, "a classify workgroup is one group of blocks");
+    if (lane_id() == 0) {
+        if (b * kWideBlock < n) {
+            parts.cnt[b] = (int32_t)kc;
+            parts.len[b] = l;
+        }
+        sm.wl[w] = kc;                  // the search's LDS is free again
+        sm.wh[w] = (uint64_t)l;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t gc = 0;
+        int64_t gl = 0;
+        for (int k = 0; k < kGroupBlocks; ++k) {
+            gc += (uint32_t)sm.wl[k];
+            gl += (int64_t)sm.wh[k];
+        }
+        parts.gcnt[blockIdx.x] = (int32_t)gc;
+        parts.glen[blockIdx.x] = gl;
     }
 }
 
@@ -557,8 +572,10 @@ int64_t wide_hist_wgs(int64_t n) {
 size_t wide_select_ws_bytes(int64_t n) {
     const int64_t mm = (n + kMMT - 1) / kMMT;
     const int64_t nb = (n + kWideBlock - 1) / kWideBlock;
+    const int64_t ng = wide_groups(n);
     return 256 + align256((size_t)mm * 8) * 2 + align256((size_t)kHBins * 4) + align256((size_t)n * 2) +
-           align256((size_t)nb * 4) * 2 + align256((size_t)nb * 8);
+           align256((size_t)nb * 4) * 2 + align256((size_t)nb * 8) + align256((size_t)ng * 4) +
+           align256((size_t)ng * 8);
 }
 
 WideWs wide_ws_carve(void *ws, int64_t n) {
@@ -574,7 +591,10 @@ WideWs wide_ws_carve(void *ws, int64_t n) {
     const int64_t nb = (n + kWideBlock - 1) / kWideBlock;
     w.parts.cnt = (int32_t *)p; p += align256((size_t)nb * 4);
     w.parts.len = (int64_t *)p; p += align256((size_t)nb * 8);
-    w.parts.pcs = (int32_t *)p;
+    w.parts.pcs = (int32_t *)p; p += align256((size_t)nb * 4);
+    const int64_t ng = wide_groups(n);
+    w.parts.gcnt = (int32_t *)p; p += align256((size_t)ng * 4);
+    w.parts.glen = (int64_t *)p;
     w.n_mm = mm;
     return w;
 }
