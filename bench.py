@@ -66,10 +66,11 @@ def parse():
 
 # (timer phase, kernel) of the fused step's launches: pools of up to 8192
 # trajectories (rank path), and larger ones (level-0 histogram of the cut
-# search, cut-and-classify, compaction with blocks of 64 trajectories)
+# search, cut-and-classify, merge-path compaction over blocks of 64
+# trajectories)
 PHASES = ((0, "score_reduce"), (1, "score_finalize"), (2, "rank"), (3, "compact_piece"))
 PHASES_WIDE = ((0, "score_reduce"), (1, "score_finalize"), (2, "cut_hist"), (6, "classify"),
-               (3, "compact_piece"))
+               (3, "compact_wide"))
 
 
 def cpu_model():
@@ -108,10 +109,12 @@ def kernel_bytes(pool, n_keep_tok, col_bytes, W, use_prefix, cus):
                    histogram (8 KiB) added;
     classify       score 8 B, offsets 16 B and digit 2 B read, keep flag 1 B
                    written per trajectory, the histogram read, the block
-                   partials (16 B per 64 trajectories) written;
+                   partials (16 B per 64 trajectories) and their group sums
+                   (16 B per 1024 trajectories) written;
     compact_piece  every kept element of each column read and written, keep
-                   flags and offsets (17 B per trajectory), the block
-                   partials, packed offsets (8 B) and kept ids (4 B) per kept
+    compact_wide   flags and offsets (17 B per trajectory), the block
+                   partials (and, for compact_wide, their group sums) read,
+                   packed offsets (8 B) and kept ids (4 B) per kept
                    trajectory and rejected ids (4 B per rejection) written."""
     n, N = pool.n, pool.n_tokens
     chunks = reduce_chunks(N, cus)
@@ -119,6 +122,7 @@ def kernel_bytes(pool, n_keep_tok, col_bytes, W, use_prefix, cus):
     blk = 64 if wide else 16
     blocks = -(-n // blk)
     groups = -(-n // 128)
+    bgroups = -(-n // 1024)
     budget = max(0, pool.occupancy - pool.capacity)
     kept = n - min(budget, n)
     pre = (8 * n + 8 * W) if use_prefix else 0
@@ -127,9 +131,10 @@ def kernel_bytes(pool, n_keep_tok, col_bytes, W, use_prefix, cus):
         "score_finalize": 16 * n + 4 * n + pre + 16 * n + 16 * chunks + 8 * n + 16 * n + (16 * groups if wide else 0),
         "rank": 8 * n + 16 * n + n + 16 * blocks,
         "cut_hist": 8 * n + 2 * n + 16 * groups + 8192,
-        "classify": 8 * n + 16 * n + 2 * n + n + 8192 + 16 * blocks,
-        "compact_piece": sum(2 * e * n_keep_tok for e in col_bytes) + 17 * n + 16 * blocks
-                         + 12 * kept + 8 + 4 * budget,
+        "classify": 8 * n + 16 * n + 2 * n + n + 8192 + 16 * blocks + 16 * bgroups,
+        "compact_wide" if wide else "compact_piece":
+            sum(2 * e * n_keep_tok for e in col_bytes) + 17 * n + 16 * blocks
+            + (16 * bgroups if wide else 0) + 12 * kept + 8 + 4 * budget,
     }
 
 
