@@ -14,10 +14,11 @@
 // called in sequence, in four launches instead of six. Pools beyond the rank
 // kernel's limit (8192 trajectories) take the selection spread over the chip
 // instead of the rank (select_wide.hip: the finalize also writes per-group
-// key extremes, then cut_hist, cut_select and classify, which writes the
-// keep flags and the partials of blocks of 64 trajectories) and the same
-// piece compaction; pools beyond that path's limit use the separate calls'
-// kernels.
+// key extremes and clears the level-0 histogram, then cut_hist, and classify,
+// where every workgroup finds the cut and writes keep flags, the partials of
+// blocks of 64 trajectories and their group sums) and compact_wide (an even
+// merge-path split of the packed output); pools beyond that path's limit use
+// the separate calls' kernels.
 #include "device_util.hpp"
 #include "kernels.hpp"
 
