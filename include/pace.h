@@ -191,7 +191,10 @@ int pace_validate(const int32_t *tags, const int64_t *offsets, int64_t n_traj, i
  * in sequence (every output is bit-identical to theirs). The device work is
  * four dependent launches instead of six: the rank kernel also writes the
  * per-block partials the compaction needs, and the compaction writes the
- * rejected ids. Pools above 8192 trajectories run the separate kernels.
+ * rejected ids. Pools of 8192 < n_traj <= 262144 select across the whole
+ * device (a level-0 histogram, then a kernel that finds the cut and writes
+ * the keep flags and partials: five launches); larger pools run the separate
+ * calls' kernels.
  *
  * occupancy, capacity, r_hat_inout, budget_out: as pace_budget ([host]).
  * score_out, gen_sum_out, gen_count_out: as pace_score (gen_* may be NULL).
