@@ -561,17 +561,6 @@ __device__ __forceinline__ void copy_spans_col(const CompactCols &cols, int col,
     }
 }
 
-// Inclusive scan inside each row of 16 lanes (row_shr 1, 2, 4, 8).
-__device__ __forceinline__ int64_t row_incl_scan_i64(int64_t v) {
-    auto add = [](uint64_t a, uint64_t b) { return a + b; };
-    uint64_t x = (uint64_t)v;
-    x = add(x, dpp_u64<0x111, 0xf>(0ull, x));
-    x = add(x, dpp_u64<0x112, 0xf>(0ull, x));
-    x = add(x, dpp_u64<0x114, 0xf>(0ull, x));
-    x = add(x, dpp_u64<0x118, 0xf>(0ull, x));
-    return (int64_t)x;
-}
-
 // One workgroup of 1024 threads per kGroupBlocks blocks of kWideBlock
 // trajectories (one wave each): the block partials from the keep flags and
 // the group's sums.

@@ -71,6 +71,23 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
 __device__ __forceinline__ int64_t wave_incl_scan_i64(int64_t v) {
     return (int64_t)wave_scan_u64((uint64_t)v, 0ull, [](uint64_t a, uint64_t b) { return a + b; });
 }
+// Inclusive scans inside each row of 16 lanes (row_shr 1, 2, 4, 8): lane
+// 16 r + 15 ends with the sum of its row.
+__device__ __forceinline__ int64_t row_incl_scan_i64(int64_t v) {
+    uint64_t x = (uint64_t)v;
+    x += dpp_u64<0x111, 0xf>(0ull, x);
+    x += dpp_u64<0x112, 0xf>(0ull, x);
+    x += dpp_u64<0x114, 0xf>(0ull, x);
+    x += dpp_u64<0x118, 0xf>(0ull, x);
+    return (int64_t)x;
+}
+__device__ __forceinline__ uint32_t row_incl_scan_u32(uint32_t x) {
+    x += dpp_u32<0x111, 0xf>(0u, x);
+    x += dpp_u32<0x112, 0xf>(0u, x);
+    x += dpp_u32<0x114, 0xf>(0u, x);
+    x += dpp_u32<0x118, 0xf>(0u, x);
+    return x;
+}
 // Wave-wide reductions, broadcast to every lane.
 __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
     return (uint64_t)readlane_i64((int64_t)wave_scan_u64(v, 0ull, [](uint64_t a, uint64_t b) { return a + b; }), kWave - 1);

@@ -7,6 +7,7 @@
 // so malformed ones give unspecified results but no out-of-bounds access.
 #include "../../include/pace.h"
 #include "device_util.hpp"
+#include "group_math.hpp"
 #include "kernels.hpp"
 
 #pragma clang fp contract(off)
@@ -23,10 +24,7 @@ __global__ __launch_bounds__(256) void group_score_kernel(const double *__restri
                                                          double *__restrict__ out) {
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (g >= ng) return;
-    const int64_t lo = clamp64(go[g], 0, n), hi = clamp64(go[g + 1], 0, n);
-    double sum = 0.0;
-    for (int64_t i = lo; i < hi; ++i) sum = sum + score[i];
-    out[g] = (hi > lo) ? sum / (double)(hi - lo) : 0.0;
+    out[g] = group_mean(score, n, go, g);
 }
 
 // One wave per group: every member takes its group's keep flag.
@@ -38,6 +36,97 @@ __global__ __launch_bounds__(256) void group_expand_kernel(const int64_t *__rest
     const int64_t lo = clamp64(go[g], 0, n), hi = clamp64(go[g + 1], 0, n);
     const uint8_t k = gkeep[g] ? 1 : 0;
     for (int64_t i = lo + lane_id(); i < hi; i += kWave) keep[i] = k;
+}
+
+// After the rank over groups, in the group filter step: workgroup w writes
+// the keep flags of trajectories [1024 w, 1024 w + 1024) (their group's
+// flag), the compaction's partials of the kPieceBlock-trajectory blocks among
+// them, and the rejected ids among groups [1024 w, 1024 w + 1024), ascending
+// (at most `budget` of them, as pace_select writes them). A trajectory's
+// group is the last group whose first member is at or before it; wave 0
+// finds that of the workgroup's first trajectory, the next kAdmStage group
+// offsets are staged in LDS, and every thread searches them (the global
+// offsets when its group lies beyond).
+constexpr int kAdmT = 1024;
+constexpr int kAdmStage = 2048;
+__global__ __launch_bounds__(kAdmT) void group_admit_kernel(const int64_t *__restrict__ go, int64_t ng, int64_t n,
+                                                           const uint8_t *__restrict__ gkeep,
+                                                           const int64_t *__restrict__ off, int64_t NT,
+                                                           uint8_t *__restrict__ keep, PieceParts parts,
+                                                           int32_t *__restrict__ reject_gids, int64_t budget) {
+    __shared__ int64_t s_go[kAdmStage + 1];
+    __shared__ int64_t s_gs;
+    __shared__ uint32_t wsum[kAdmT / kWave];
+    const int t = threadIdx.x, lane = lane_id();
+    const int64_t a = (int64_t)blockIdx.x * kAdmT;
+    const int64_t i = a + t;
+
+    // Loads that need no search: the trajectory's span, the rejected-group
+    // flags before this workgroup's groups (strided) and its own group flag.
+    int64_t span = 0;
+    if (i < n) {
+        const int64_t lo = clamp64(off[i], 0, NT), hi = clamp64(off[i + 1], 0, NT);
+        span = hi > lo ? hi - lo : 0;
+    }
+    const int64_t a_g = a < ng ? a : ng;
+    uint32_t before = 0;
+    for (int64_t k = t; k < a_g; k += kAdmT) before += gkeep[k] == 0 ? 1u : 0u;
+    const int64_t gr = a + t;
+    const bool rej = gr < ng && gkeep[gr] == 0;
+
+    // The group of trajectory a, then the staged group offsets.
+    if (ng > 0 && a < n && t < kWave) {
+        int64_t gs = wave_last_le(go, ng - 1, a);
+        gs = gs < 0 ? 0 : gs;
+        if (t == 0) s_gs = gs;
+    }
+    // Rejected ids: rej | (strided count << 11) in one block sum (the
+    // workgroup holds at most 1024 rejected groups: 11 bits).
+    uint32_t tot;
+    const uint32_t ex = block_excl_sum_u32<kAdmT / kWave>((rej ? 1u : 0u) | (before << 11), tot, wsum);
+    if (rej && reject_gids) {
+        const int64_t pos = (int64_t)(tot >> 11) + (int64_t)(ex & 2047u);
+        if (pos < budget) reject_gids[pos] = (int32_t)gr;
+    }
+    if (ng == 0 || a >= n) return;            // no trajectory here (block-uniform)
+    const int64_t gs = s_gs;
+    const int64_t m = (ng - gs < kAdmStage) ? ng - gs : kAdmStage;   // s_go[0..m] = go[gs..gs+m]
+    for (int64_t k = t; k <= m; k += kAdmT) s_go[k] = go[gs + k];
+    __syncthreads();
+
+    bool kept = false;
+    if (i < n) {
+        // last k in [0, m) with s_go[k] <= i (s_go[0] <= a <= i for well-formed offsets)
+        int64_t lo = 0, hi = m;
+        while (hi - lo > 1) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (s_go[mid] <= i) lo = mid; else hi = mid;
+        }
+        int64_t g = gs + lo;
+        if (m < ng - gs && s_go[m] <= i) {    // beyond the staged offsets: search the rest
+            int64_t l2 = gs + m, h2 = ng;
+            while (h2 - l2 > 1) {
+                const int64_t mid = (l2 + h2) >> 1;
+                if (go[mid] <= i) l2 = mid; else h2 = mid;
+            }
+            g = l2;
+        }
+        kept = gkeep[g] != 0;
+        keep[i] = kept ? 1 : 0;
+    }
+
+    // Block partials: rows of 16 lanes are blocks of kPieceBlock trajectories.
+    static_assert(kPieceBlock == 16 && kAdmT % kPieceBlock == 0, "a block is one row of 16 lanes");
+    const int64_t len = kept ? span : 0;
+    const int64_t l_row = row_incl_scan_i64(len);
+    const uint32_t p_row = row_incl_scan_u32((uint32_t)((len + kPieceLen - 1) / kPieceLen));
+    const uint32_t c_row = (uint32_t)__popcll((ballot(kept) >> (lane & ~15)) & 0xffffull);
+    const int64_t b = i / kPieceBlock;
+    if ((lane & 15) == 15 && b * kPieceBlock < n) {
+        parts.cnt[b] = (int32_t)c_row;
+        parts.len[b] = l_row;
+        parts.pcs[b] = (int32_t)p_row;
+    }
 }
 
 __global__ void group_validate_init_kernel(int32_t *err) { *err = 0; }
@@ -66,6 +155,16 @@ hipError_t launch_group_expand(const int64_t *group_offsets, int64_t ng, int64_t
     if (ng == 0 || n == 0) return hipSuccess;
     return launch(kPhaseAux, group_expand_kernel, dim3((unsigned)((ng + 3) / 4)), dim3(256), stream, group_offsets,
                   ng, n, group_keep, keep);
+}
+
+hipError_t launch_group_admit(const int64_t *group_offsets, int64_t ng, int64_t n, const uint8_t *group_keep,
+                              const int64_t *offsets, int64_t n_tokens, uint8_t *keep, const PieceParts &parts,
+                              int32_t *reject_group_ids, int64_t budget, hipStream_t stream) {
+    const int64_t items = n > ng ? n : ng;
+    const int64_t wgs = items > 0 ? (items + kAdmT - 1) / kAdmT : 0;
+    if (wgs == 0) return hipSuccess;
+    return launch(kPhaseAux, group_admit_kernel, dim3((unsigned)wgs), dim3(kAdmT), stream, group_offsets, ng, n,
+                  group_keep, offsets, n_tokens, keep, parts, reject_group_ids, budget);
 }
 
 hipError_t launch_group_validate(const int64_t *group_offsets, int64_t ng, int64_t n, int32_t *err,
@@ -97,6 +196,18 @@ hipError_t launch_group_filter_step(const int32_t *tags, const int64_t *offsets,
     hipError_t e = launch_score(tags, offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix,
                                 w_wait, gamma, score, gen_sum, gen_count, sws, vec_ok, stream);
     if (e != hipSuccess) return e;
+    if (ng <= kRankMaxN && compact_piece_ok(n, n_tokens)) {
+        // Group scores inside the rank over groups; one kernel for the
+        // members' flags, the compaction's partials and the rejected ids.
+        const CompactWs cw = compact_ws_carve(cws, N, n_tokens);
+        e = launch_group_rank(score, n, group_offsets, ng, budget, group_score, group_keep, stream);
+        if (e != hipSuccess) return e;
+        e = launch_group_admit(group_offsets, ng, n, group_keep, offsets, n_tokens, keep, cw.parts,
+                               reject_group_ids, budget, stream);
+        if (e != hipSuccess) return e;
+        return launch_compact_pieces(offsets, n, n_tokens, keep, cw.parts, cols, n_cols, offsets_out, kept_ids,
+                                     n_kept_tokens, nullptr, 0, n, stream);
+    }
     e = launch_group_score(score, n, group_offsets, ng, group_score, stream);
     if (e != hipSuccess) return e;
     e = launch_select(group_score, ng, budget, group_keep, reject_group_ids, sel_ws, stream);

@@ -154,6 +154,10 @@ hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const
 
 // keep[i] <- 0 for the `budget` first trajectories in (score desc, id asc).
 // With parts.cnt non-null, also writes the block partials of the keep flags.
+// Group means of pace_group_score formed inside the rank over groups (at
+// most kRankMaxN groups): group scores and group keep flags in one launch.
+hipError_t launch_group_rank(const double *score, int64_t n, const int64_t *group_offsets, int64_t ng,
+                             int64_t budget, double *group_score, uint8_t *group_keep, hipStream_t stream);
 hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,
                        const int64_t *offsets, int64_t n_tokens, const PieceParts &parts,
                        hipStream_t stream);

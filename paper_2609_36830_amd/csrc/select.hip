@@ -16,6 +16,7 @@
 // ordered count.
 #include "device_util.hpp"
 #include "kernels.hpp"
+#include "group_math.hpp"
 #include "select_block.hpp"
 
 namespace pace {
@@ -233,31 +234,16 @@ __device__ __forceinline__ uint32_t rank_add_beats(uint32_t c, const RankKey &a,
     return c;
 }
 
+// Ranks the kRankQ targets i0 .. i0 + kRankQ - 1 of this workgroup against
+// all n keys and writes their keep flags (and, with parts.cnt, the block's
+// partials). v[u]: the score of item t + u * kRankT; kq_lane: in lanes
+// q < kRankQ of every wave, the key of target i0 + q; span: in threads
+// t < kRankQ, the clamped span length of target i0 + t.
 template <int kKeys>
-__global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__ score, int64_t n,
-                                                     int64_t budget, uint8_t *__restrict__ keep,
-                                                     const int64_t *__restrict__ off, int64_t NT,
-                                                     PieceParts parts) {
-    __shared__ uint32_t part[kRankT / kWave][kRankQ];
+__device__ __forceinline__ void rank_block(const double (&v)[kKeys], uint64_t kq_lane, int64_t i0, int64_t n,
+                                           int64_t budget, uint8_t *__restrict__ keep, int64_t span,
+                                           const PieceParts &parts, uint32_t (*part)[kRankQ]) {
     const int t = threadIdx.x;
-    const int64_t i0 = (int64_t)blockIdx.x * kRankQ;
-    // All loads first: this thread's keys, the targets, the block's spans.
-    double v[kKeys];
-#pragma unroll
-    for (int u = 0; u < kKeys; ++u) {
-        const int64_t j = t + (int64_t)u * kRankT;
-        v[u] = j < n ? score[j] : 0.0;
-    }
-    // Lane q of every wave loads target q; its key is formed in the vector
-    // unit and read out to scalars (a scalar-side conversion branches on
-    // every target).
-    const int lane = lane_id();
-    const double vq = lane < kRankQ && i0 + lane < n ? score[i0 + lane] : 0.0;
-    int64_t span = 0;
-    if (parts.cnt && t < kRankQ && i0 + t < n) {
-        const int64_t lo = clamp64(off[i0 + t], 0, NT), hi = clamp64(off[i0 + t + 1], 0, NT);
-        span = hi > lo ? hi - lo : 0;
-    }
     // Padding keys are 0: below every target key (the smallest key of a
     // number is that of -inf, above 0), so they never count.
     uint64_t kj[kKeys];
@@ -266,7 +252,6 @@ __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__
         const int64_t j = t + (int64_t)u * kRankT;
         kj[u] = j < n ? score_key(v[u]) : 0ull;
     }
-    const uint64_t kq_lane = score_key(vq);
     uint64_t kq[kRankQ], kq_m1[kRankQ];
 #pragma unroll
     for (int q = 0; q < kRankQ; ++q) {
@@ -343,6 +328,69 @@ __global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__
     }
 }
 
+
+template <int kKeys>
+__global__ __launch_bounds__(kRankT) void rank_kernel(const double *__restrict__ score, int64_t n,
+                                                     int64_t budget, uint8_t *__restrict__ keep,
+                                                     const int64_t *__restrict__ off, int64_t NT,
+                                                     PieceParts parts) {
+    __shared__ uint32_t part[kRankT / kWave][kRankQ];
+    const int t = threadIdx.x;
+    const int64_t i0 = (int64_t)blockIdx.x * kRankQ;
+    // All loads first: this thread's keys, the targets, the block's spans.
+    double v[kKeys];
+#pragma unroll
+    for (int u = 0; u < kKeys; ++u) {
+        const int64_t j = t + (int64_t)u * kRankT;
+        v[u] = j < n ? score[j] : 0.0;
+    }
+    // Lane q of every wave loads target q; its key is formed in the vector
+    // unit and read out to scalars (a scalar-side conversion branches on
+    // every target).
+    const int lane = lane_id();
+    const double vq = lane < kRankQ && i0 + lane < n ? score[i0 + lane] : 0.0;
+    int64_t span = 0;
+    if (parts.cnt && t < kRankQ && i0 + t < n) {
+        const int64_t lo = clamp64(off[i0 + t], 0, NT), hi = clamp64(off[i0 + t + 1], 0, NT);
+        span = hi > lo ? hi - lo : 0;
+    }
+    rank_block<kKeys>(v, score_key(vq), i0, n, budget, keep, span, parts, part);
+}
+
+// Prompt groups (at most kRankMaxN) in the group filter step: every
+// workgroup forms all ng group means from the trajectory scores (group_mean,
+// the arithmetic of pace_group_score) and ranks its kRankQ target groups
+// against them, writing the targets' group scores and keep flags. Forming
+// the means in every workgroup costs ng / kRankQ times the loads of one pass
+// over the scores, and saves the group scores' launch.
+template <int kKeys>
+__global__ __launch_bounds__(kRankT) void group_rank_kernel(const double *__restrict__ score, int64_t n,
+                                                           const int64_t *__restrict__ go, int64_t ng,
+                                                           int64_t budget, double *__restrict__ group_score,
+                                                           uint8_t *__restrict__ group_keep) {
+    __shared__ uint32_t part[kRankT / kWave][kRankQ];
+    __shared__ uint64_t s_key[kRankQ];
+    const int t = threadIdx.x;
+    const int64_t i0 = (int64_t)blockIdx.x * kRankQ;
+    double v[kKeys];
+#pragma unroll
+    for (int u = 0; u < kKeys; ++u) {
+        const int64_t g = t + (int64_t)u * kRankT;
+        v[u] = 0.0;
+        if (g < ng) {
+            v[u] = group_mean(score, n, go, g);
+            if (g >= i0 && g < i0 + kRankQ) {   // this workgroup's targets
+                group_score[g] = v[u];
+                s_key[g - i0] = score_key(v[u]);
+            }
+        }
+    }
+    __syncthreads();
+    const int lane = lane_id();
+    const uint64_t kq_lane = (lane < kRankQ && i0 + lane < ng) ? s_key[lane] : 0ull;
+    rank_block<kKeys>(v, kq_lane, i0, ng, budget, group_keep, 0, PieceParts{}, part);
+}
+
 // Rejected ids in ascending order from the keep flags (n <= 1024*kItems).
 template <int kItems>
 __global__ __launch_bounds__(kT) void emit_rejects_kernel(const uint8_t *__restrict__ keep, int64_t n,
@@ -389,6 +437,21 @@ hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *
     if (n <= 4 * kRankT) PACE_RANK(4);
     PACE_RANK(8);
 #undef PACE_RANK
+}
+
+hipError_t launch_group_rank(const double *score, int64_t n, const int64_t *group_offsets, int64_t ng,
+                             int64_t budget, double *group_score, uint8_t *group_keep, hipStream_t stream) {
+    if (ng == 0) return hipSuccess;
+    if (ng > kRankMaxN) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)((ng + kRankQ - 1) / kRankQ));
+#define PACE_GROUP_RANK(K) \
+    return launch(kPhaseSelect, group_rank_kernel<K>, grid, dim3(kRankT), stream, score, n, group_offsets, ng, \
+                  budget, group_score, group_keep)
+    if (ng <= kRankT) PACE_GROUP_RANK(1);
+    if (ng <= 2 * kRankT) PACE_GROUP_RANK(2);
+    if (ng <= 4 * kRankT) PACE_GROUP_RANK(4);
+    PACE_GROUP_RANK(8);
+#undef PACE_GROUP_RANK
 }
 
 hipError_t launch_select(const double *score, int64_t n, int64_t budget, uint8_t *keep,
