@@ -2,6 +2,7 @@
 prompt groups; groups budgeted, selected and compacted as units): the HIP
 library through the C ABI against the CPU oracle, bit-exact (group scores
 too: both sides add the members in order and divide once)."""
+import dataclasses
 import sys
 
 import numpy as np
@@ -131,6 +132,33 @@ def test_group_step_more_groups_than_trajectories(pace):
     assert ng > pool.n
     say("group step tiny pool, %d groups over %d trajectories" % (ng, pool.n))
     group_step_parity(pace, pool, go, ng, ng // 2)
+
+
+@pytest.mark.parametrize("empties,label", [(6, "7 groups per trajectory, under the 8192-group limit"),
+                                           (8, "9 groups per trajectory, past the limit")])
+def test_group_step_many_empty_groups(pace, empties, label):
+    # Each of the math pool's 1024 trajectories follows `empties` empty
+    # groups: 1024 trajectories then span more group offsets than one
+    # workgroup stages (so threads search the global offsets too), and 9 per
+    # trajectory take the group count past the fused step's limit.
+    pool = poolgen.make_pool("math")
+    sizes = np.tile(np.array([0] * empties + [1], np.int64), pool.n)
+    go = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int64)
+    ng = len(go) - 1
+    say("group step math pool, %d groups (%s)" % (ng, label))
+    o = group_step_parity(pace, pool, go, ng, ng - 512)
+    assert 0 < int(o["keep"].sum()) < pool.n
+
+
+def test_group_step_no_trajectories(pace):
+    # Every group empty: the group scores are 0, the rejected ids are the
+    # lowest ids, and nothing is packed.
+    pool = poolgen.make_pool("tiny")
+    empty = dataclasses.replace(pool, tags=pool.tags[:0], offsets=np.zeros(1, np.int64),
+                                completion=pool.completion[:0], prefix_score=pool.prefix_score[:0])
+    go = np.zeros(40, np.int64)
+    say("group step, 39 empty groups and no trajectories")
+    group_step_parity(pace, empty, go, 39, 20)
 
 
 @pytest.mark.parametrize("occ,cap", [(10, 20), (64, 0), (64, 63)])
