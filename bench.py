@@ -170,10 +170,10 @@ def reduce_traffic(config, cols):
 
 # config -> {"sha256": digest of the score_reduce sources, "bytes": HBM bytes per launch}
 REDUCE_COUNTERS = {
-    # profiles/filter_step_hbm_counters.md: FETCH_SIZE 98216.9 KiB, WRITE_SIZE 170.3 KiB
-    "stress": {"sha256": "6b5c5dfd5e03cd9fd343fb9ff0ba575baf1ca44aab45fa50b70d3c78ff25f158", "bytes": 201322598},
-    # profiles/filter_step_hbm_counters.md: FETCH_SIZE 103519.3 KiB, WRITE_SIZE 1138.9 KiB
-    "wide": {"sha256": "6b5c5dfd5e03cd9fd343fb9ff0ba575baf1ca44aab45fa50b70d3c78ff25f158", "bytes": 213173760},
+    # profiles/filter_step_hbm_counters.md: FETCH_SIZE 98218.9 KiB, WRITE_SIZE 170.2 KiB
+    "stress": {"sha256": "97cdaed24ff7101054241bfed79d2b19a6fa70afd19992b81495cc102254f5b9", "bytes": 201326592},
+    # profiles/filter_step_hbm_counters.md: FETCH_SIZE 103516.6 KiB, WRITE_SIZE 1139.1 KiB
+    "wide": {"sha256": "97cdaed24ff7101054241bfed79d2b19a6fa70afd19992b81495cc102254f5b9", "bytes": 213168435},
 }
 
 
