@@ -47,8 +47,13 @@ __global__ __launch_bounds__(256) void group_expand_kernel(const int64_t *__rest
 // finds that of the workgroup's first trajectory, the next kAdmStage group
 // offsets are staged in LDS, and every thread searches them (the global
 // offsets when its group lies beyond).
+// kWide: the partials of blocks of kWideBlock trajectories (one wave) and
+// their sums per workgroup (one group of kGroupBlocks blocks), the two
+// levels the merge-path compaction reads; else blocks of kPieceBlock.
 constexpr int kAdmT = 1024;
 constexpr int kAdmStage = 2048;
+static_assert(kAdmT == kWideBlock * kGroupBlocks, "a workgroup is one group of wide blocks");
+template <bool kWide>
 __global__ __launch_bounds__(kAdmT) void group_admit_kernel(const int64_t *__restrict__ go, int64_t ng, int64_t n,
                                                            const uint8_t *__restrict__ gkeep,
                                                            const int64_t *__restrict__ off, int64_t NT,
@@ -57,6 +62,7 @@ __global__ __launch_bounds__(kAdmT) void group_admit_kernel(const int64_t *__res
     __shared__ int64_t s_go[kAdmStage + 1];
     __shared__ int64_t s_gs;
     __shared__ uint32_t wsum[kAdmT / kWave];
+    __shared__ int64_t wlen[kAdmT / kWave];
     const int t = threadIdx.x, lane = lane_id();
     const int64_t a = (int64_t)blockIdx.x * kAdmT;
     const int64_t i = a + t;
@@ -115,17 +121,46 @@ __global__ __launch_bounds__(kAdmT) void group_admit_kernel(const int64_t *__res
         keep[i] = kept ? 1 : 0;
     }
 
-    // Block partials: rows of 16 lanes are blocks of kPieceBlock trajectories.
-    static_assert(kPieceBlock == 16 && kAdmT % kPieceBlock == 0, "a block is one row of 16 lanes");
     const int64_t len = kept ? span : 0;
-    const int64_t l_row = row_incl_scan_i64(len);
-    const uint32_t p_row = row_incl_scan_u32((uint32_t)((len + kPieceLen - 1) / kPieceLen));
-    const uint32_t c_row = (uint32_t)__popcll((ballot(kept) >> (lane & ~15)) & 0xffffull);
-    const int64_t b = i / kPieceBlock;
-    if ((lane & 15) == 15 && b * kPieceBlock < n) {
-        parts.cnt[b] = (int32_t)c_row;
-        parts.len[b] = l_row;
-        parts.pcs[b] = (int32_t)p_row;
+    if constexpr (kWide) {
+        // A wave is a block of kWideBlock trajectories; the workgroup is
+        // their group.
+        static_assert(kWideBlock == kWave, "a wide block is one wave");
+        const uint32_t c = (uint32_t)__popcll(ballot(kept));
+        const int64_t l = wave_sum_i64(len);
+        const int w = t / kWave;
+        const int64_t b = i / kWideBlock;
+        if (lane == 0) {
+            if (b * kWideBlock < n) {
+                parts.cnt[b] = (int32_t)c;
+                parts.len[b] = l;
+            }
+            wsum[w] = c;
+            wlen[w] = l;
+        }
+        __syncthreads();
+        if (t == 0) {
+            uint32_t gc = 0;
+            int64_t gl = 0;
+            for (int k = 0; k < kAdmT / kWave; ++k) {
+                gc += wsum[k];
+                gl += wlen[k];
+            }
+            parts.gcnt[blockIdx.x] = (int32_t)gc;
+            parts.glen[blockIdx.x] = gl;
+        }
+    } else {
+        // Rows of 16 lanes are blocks of kPieceBlock trajectories.
+        static_assert(kPieceBlock == 16 && kAdmT % kPieceBlock == 0, "a block is one row of 16 lanes");
+        const int64_t l_row = row_incl_scan_i64(len);
+        const uint32_t p_row = row_incl_scan_u32((uint32_t)((len + kPieceLen - 1) / kPieceLen));
+        const uint32_t c_row = (uint32_t)__popcll((ballot(kept) >> (lane & ~15)) & 0xffffull);
+        const int64_t b = i / kPieceBlock;
+        if ((lane & 15) == 15 && b * kPieceBlock < n) {
+            parts.cnt[b] = (int32_t)c_row;
+            parts.len[b] = l_row;
+            parts.pcs[b] = (int32_t)p_row;
+        }
     }
 }
 
@@ -159,12 +194,15 @@ hipError_t launch_group_expand(const int64_t *group_offsets, int64_t ng, int64_t
 
 hipError_t launch_group_admit(const int64_t *group_offsets, int64_t ng, int64_t n, const uint8_t *group_keep,
                               const int64_t *offsets, int64_t n_tokens, uint8_t *keep, const PieceParts &parts,
-                              int32_t *reject_group_ids, int64_t budget, hipStream_t stream) {
+                              int32_t *reject_group_ids, int64_t budget, bool wide, hipStream_t stream) {
     const int64_t items = n > ng ? n : ng;
     const int64_t wgs = items > 0 ? (items + kAdmT - 1) / kAdmT : 0;
     if (wgs == 0) return hipSuccess;
-    return launch(kPhaseAux, group_admit_kernel, dim3((unsigned)wgs), dim3(kAdmT), stream, group_offsets, ng, n,
-                  group_keep, offsets, n_tokens, keep, parts, reject_group_ids, budget);
+    if (wide)
+        return launch(kPhaseAux, group_admit_kernel<true>, dim3((unsigned)wgs), dim3(kAdmT), stream, group_offsets,
+                      ng, n, group_keep, offsets, n_tokens, keep, parts, reject_group_ids, budget);
+    return launch(kPhaseAux, group_admit_kernel<false>, dim3((unsigned)wgs), dim3(kAdmT), stream, group_offsets, ng,
+                  n, group_keep, offsets, n_tokens, keep, parts, reject_group_ids, budget);
 }
 
 hipError_t launch_group_validate(const int64_t *group_offsets, int64_t ng, int64_t n, int32_t *err,
@@ -196,17 +234,19 @@ hipError_t launch_group_filter_step(const int32_t *tags, const int64_t *offsets,
     hipError_t e = launch_score(tags, offsets, n, n_tokens, completion, V, prefix, window, W, use_prefix,
                                 w_wait, gamma, score, gen_sum, gen_count, sws, vec_ok, stream);
     if (e != hipSuccess) return e;
-    if (ng <= kRankMaxN && compact_piece_ok(n, n_tokens)) {
+    const bool pieces = compact_piece_ok(n, n_tokens);
+    if (ng <= kRankMaxN && (pieces || compact_wide_ok(n, n_tokens))) {
         // Group scores inside the rank over groups; one kernel for the
-        // members' flags, the compaction's partials and the rejected ids.
+        // members' flags, the compaction's partials (blocks of 16, or of 64
+        // with group sums for the merge-path compaction) and the rejected ids.
         const CompactWs cw = compact_ws_carve(cws, N, n_tokens);
         e = launch_group_rank(score, n, group_offsets, ng, budget, group_score, group_keep, stream);
         if (e != hipSuccess) return e;
         e = launch_group_admit(group_offsets, ng, n, group_keep, offsets, n_tokens, keep, cw.parts,
-                               reject_group_ids, budget, stream);
+                               reject_group_ids, budget, !pieces, stream);
         if (e != hipSuccess) return e;
         return launch_compact_pieces(offsets, n, n_tokens, keep, cw.parts, cols, n_cols, offsets_out, kept_ids,
-                                     n_kept_tokens, nullptr, 0, n, stream);
+                                     n_kept_tokens, nullptr, 0, n, stream, pieces ? kPieceBlock : kWideBlock);
     }
     e = launch_group_score(score, n, group_offsets, ng, group_score, stream);
     if (e != hipSuccess) return e;

@@ -150,6 +150,23 @@ def test_group_step_many_empty_groups(pace, empties, label):
     assert 0 < int(o["keep"].sum()) < pool.n
 
 
+@pytest.mark.parametrize("n,size", [(16384, 8), (65536, 8), (20000, 3)])
+def test_group_step_wide_pools(pace, n, size):
+    # Past 8192 trajectories the compaction takes blocks of 64 with group
+    # sums (merge path); up to 8192 groups the fused group path writes them.
+    pool = poolgen.make_pool("wide", n=n)
+    rng = np.random.default_rng(n + size)
+    if size == 3:
+        go = random_groups(rng, pool.n, max_size=5, empty_frac=0.05)
+    else:
+        go = np.arange(0, pool.n + size, size, dtype=np.int64)
+        go[-1] = pool.n
+    ng = len(go) - 1
+    say("group step wide pool n=%d, %d groups" % (pool.n, ng))
+    o = group_step_parity(pace, pool, go, ng, ng // 3)
+    assert 0 < int(o["keep"].sum()) < pool.n
+
+
 def test_group_step_no_trajectories(pace):
     # Every group empty: the group scores are 0, the rejected ids are the
     # lowest ids, and nothing is packed.
