@@ -240,7 +240,15 @@ hipError_t launch_group_filter_step(const int32_t *tags, const int64_t *offsets,
         // members' flags, the compaction's partials (blocks of 16, or of 64
         // with group sums for the merge-path compaction) and the rejected ids.
         const CompactWs cw = compact_ws_carve(cws, N, n_tokens);
-        e = launch_group_rank(score, n, group_offsets, ng, budget, group_score, group_keep, stream);
+        if ((ng + kRankQ - 1) / kRankQ * n <= kGroupRankLoads) {
+            e = launch_group_rank(score, n, group_offsets, ng, budget, group_score, group_keep, stream);
+        } else {
+            // Every rank workgroup re-forming every mean would read the
+            // scores ng / kRankQ times over: form them once.
+            e = launch_group_score(score, n, group_offsets, ng, group_score, stream);
+            if (e == hipSuccess)
+                e = launch_rank(group_score, ng, budget, group_keep, nullptr, 0, PieceParts{}, stream);
+        }
         if (e != hipSuccess) return e;
         e = launch_group_admit(group_offsets, ng, n, group_keep, offsets, n_tokens, keep, cw.parts,
                                reject_group_ids, budget, !pieces, stream);

@@ -156,6 +156,11 @@ hipError_t launch_wide_cut(const double *score, int64_t n, int64_t budget, const
 // With parts.cnt non-null, also writes the block partials of the keep flags.
 // Group means of pace_group_score formed inside the rank over groups (at
 // most kRankMaxN groups): group scores and group keep flags in one launch.
+// Every rank workgroup (one per kRankQ groups) reads all member scores, so
+// the group step uses it while ceil(ng / kRankQ) * n stays within
+// kGroupRankLoads, and a separate pass of group means before the rank beyond.
+constexpr int kRankQ = 16;              // targets per rank workgroup
+constexpr int64_t kGroupRankLoads = (int64_t)1 << 21;
 hipError_t launch_group_rank(const double *score, int64_t n, const int64_t *group_offsets, int64_t ng,
                              int64_t budget, double *group_score, uint8_t *group_keep, hipStream_t stream);
 hipError_t launch_rank(const double *score, int64_t n, int64_t budget, uint8_t *keep,

@@ -205,7 +205,6 @@ __global__ __launch_bounds__(kT) void select_reg_kernel(const double *__restrict
 // traffic per pair; the n^2 comparisons spread over the whole device with no
 // dependent rounds.
 constexpr int kRankT = 1024;
-constexpr int kRankQ = 16;
 constexpr int kRankMaxKeys = (int)((kRankMaxN + kRankT - 1) / kRankT);
 
 static_assert(kRankQ == kPieceBlock, "a rank workgroup covers one partials block");
