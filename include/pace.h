@@ -407,11 +407,14 @@ int pace_diagnostics(const double *score, const int64_t *gen_sum, const int64_t 
  * thread. Calls on other threads never see it.
  * phase: PACE_PHASE_REDUCE (token reduction of pace_score), PACE_PHASE_FINALIZE
  *   (score finalisation), PACE_PHASE_SELECT (the rank kernel, the
- *   single-workgroup select of the largest pools, or the streaming draw),
+ *   single-workgroup select of the largest pools, the streaming draw, or in
+ *   pace_group_filter_step the rank over groups),
  *   PACE_PHASE_COMPACT (the compaction copy kernel), PACE_PHASE_PREFIX (the
  *   Prefix Forgetting Score kernel), PACE_PHASE_AUX (the single kernel of
  *   pace_group_score, pace_group_expand, pace_stale_k or pace_diagnostics,
- *   or the window-cutoff kernel of the streaming rule), PACE_PHASE_CLASSIFY
+ *   the window-cutoff kernel of the streaming rule, or in
+ *   pace_group_filter_step the kernel that expands the group flags),
+ *   PACE_PHASE_CLASSIFY
  *   (pools above 8192 trajectories: the kernel that finds the rejection cut
  *   and writes the keep flags; PACE_PHASE_SELECT then times the level-0
  *   histogram of that cut search).
